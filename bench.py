@@ -1,0 +1,299 @@
+"""Benchmark: spliced decode attention over a full synthetic sweep on one GPU.
+
+A "step" is one decode step of the sweep: all N layers' calls of
+splice_decode_attn (the whole hot path) for all C cells at decode position
+s.  K timed steps take s evenly spaced over [0, S) -- the default K = S is
+exactly one full sweep.  Each step's N calls are captured once in a HIP
+graph (torch.cuda.CUDAGraph) and replayed; every layer has its own caches,
+all resident in HBM before the timed region starts.
+
+Reported (one JSON line):
+  value       algorithmic bytes / wall time of the timed region (GB/s); the
+              algorithmic bytes of a call count each shared prompt tile once
+              (q, visible non-span prompt, clean span if a clean cell reads
+              it, donor span if a spliced cell reads a donor buffer, every
+              cell's visible generated rows, out and lse);
+  cell_steps_per_s   C * K / wall time;
+  roofline    bound "hbm": achieved = algorithmic bytes per launch / average
+              launch duration (HIP events on the launch stream, over the
+              timed region), peak 8000 GB/s, and the HBM traffic per launch
+              from the committed rocprofv3 counter summary when it was taken
+              on the current kernel source (else null);
+  cpu_baseline  the fp64 oracle timed on this host's cores on a stratified
+              sample of the same workload's calls.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--config qwen3-4b]
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+PROFILES = os.path.join(ROOT, "profiles")
+KERNEL_SOURCES = [os.path.join(ROOT, "paper_2605_30574_amd", "csrc", f)
+                  for f in ("splice_attn.hip", "plan.hpp")]
+
+
+def log(msg: str) -> None:
+    sys.stderr.write(f"[bench] {msg}\n")
+    sys.stderr.flush()
+
+
+def kernel_source_hash() -> str:
+    h = hashlib.sha256()
+    for p in KERNEL_SOURCES:
+        with open(p, "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+# ------------------------------------------------------------------ algorithmic bytes
+
+def call_bytes(w, layer: int, step: int, spliced_flags) -> int:
+    """Bytes a call must move at minimum: each prompt tile once per call."""
+    e = w.elem_bytes
+    row = 2 * w.n_kv_heads * w.head_dim * e            # K + V row of every KV head
+    Tp, (a, b) = w.prompt_len, w.span
+    win = w.window(layer)
+    p = Tp + step
+    j0 = p - win + 1 if win > 0 else 0
+    jp0 = min(max(j0, 0), Tp)
+    i0 = max(0, j0 - Tp)
+    n_gen = step + 1 - i0
+    sa = min(max(a, jp0), Tp)
+    sb = min(max(b, sa), Tp)
+    n_sv = sb - sa
+    n_ns = (Tp - jp0) - n_sv
+    C = w.n_cells
+    any_clean = any(not f for f in spliced_flags)
+    any_spl = any(spliced_flags)
+    buffer_donor = w.donor != "zero"
+    total = C * w.n_q_heads * w.head_dim * e                     # q
+    total += n_ns * row                                         # non-span prompt
+    total += (n_sv * row) if any_clean else 0                   # clean span
+    total += (n_sv * row) if (any_spl and buffer_donor) else 0  # donor span
+    total += C * n_gen * row                                    # generated rows
+    total += C * w.n_q_heads * (4 * w.head_dim + 4)             # out + lse
+    return total
+
+
+def spliced_flags(w, layer, step):
+    return [layer >= L and step >= W for (L, W) in w.cells]
+
+
+# ------------------------------------------------------------------ CPU baseline
+
+def cpu_baseline(w, seconds_cap: float = 30.0):
+    """Time the fp64 oracle (as it stands) on a stratified sample of calls."""
+    import numpy as np
+    import oracle
+    import workloads
+    N, S = w.n_layers, w.n_steps
+    layers = sorted({0, N // 2, N - 1})
+    n_s = min(S, 64)
+    steps = sorted({min(S - 1, int((i + 0.5) * S / n_s)) for i in range(n_s)})
+    lw = workloads.cell_lw(w)
+    osh = oracle.shape_of(w)
+    lib = oracle.load()
+    threads = oracle.max_threads()
+    done_bytes, done_time, n_calls = 0, 0.0, 0
+    t_start = time.time()
+    for layer in layers:
+        hb = {k: workloads.to_numpy(v) for k, v in workloads.make_layer(w, layer, device="cpu").items()}
+        for step in steps:
+            q = workloads.to_numpy(workloads.make_q(w, layer, step, device="cpu"))
+            t0 = time.perf_counter()
+            oracle.attn(osh, layer, step, w.window(layer), w.scale, lw, q, hb["clean_k"], hb["clean_v"],
+                        hb["donor_k"], hb["donor_v"], hb["gen_k"], hb["gen_v"], n_threads=threads, lib=lib)
+            done_time += time.perf_counter() - t0
+            done_bytes += call_bytes(w, layer, step, spliced_flags(w, layer, step))
+            n_calls += 1
+            if time.time() - t_start > seconds_cap:
+                break
+        del hb
+        if time.time() - t_start > seconds_cap:
+            break
+    gbs = done_bytes / done_time / 1e9
+    return {"value": round(gbs, 4), "unit": "GB/s", "cores": threads, "kind": "oracle",
+            "sample": f"{n_calls} calls of {w.name}: layers {layers} x {len(steps)} steps evenly "
+                      f"spaced over [0, {S}) (stratified), "
+                      f"all {w.n_cells} cells x {w.n_q_heads} heads, fp64, {done_time:.1f} s",
+            "calls": n_calls, "seconds": round(done_time, 2)}
+
+
+# ------------------------------------------------------------------ traffic from profiles
+
+def stored_traffic(w_name: str):
+    """HBM bytes per launch from the committed rocprofv3 counter summary, if it
+    was taken on the current kernel source and workload."""
+    path = os.path.join(PROFILES, f"attn_kernel_{w_name}_traffic.txt")
+    if not os.path.exists(path):
+        return None, "no counter summary"
+    fields = {}
+    for ln in open(path):
+        if ":" in ln and not ln.startswith("#"):
+            k, v = ln.split(":", 1)
+            fields[k.strip()] = v.strip()
+    if fields.get("kernel_source_sha256_16") != kernel_source_hash():
+        return None, "kernel changed since the counters were taken"
+    try:
+        return float(fields["traffic_bytes_per_launch"]), path
+    except (KeyError, ValueError):
+        return None, "malformed counter summary"
+
+
+# ------------------------------------------------------------------ main
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=0, help="timed decode steps (default: S = one sweep)")
+    ap.add_argument("--warmup", type=int, default=8)
+    ap.add_argument("--config", default="qwen3-4b")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=20.0)
+    ap.add_argument("--eager", action="store_true", help="launch without graphs")
+    ap.add_argument("--copy-calibration", type=int, default=0,
+                    help="only run a plain device copy of this many MiB (counter calibration)")
+    args = ap.parse_args()
+
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print("bench.py runs on exactly one GPU: the sweep shards cells across GPUs with no "
+              "exchange, and multi-GPU runs are not part of this build.", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import paper_2605_30574_amd as sp
+    import workloads
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+
+    if args.copy_calibration:
+        n = args.copy_calibration << 20
+        src = torch.empty(n, dtype=torch.uint8, device=dev).fill_(1)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        for _ in range(5):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_calibration_bytes": n, "launches": 5}))
+        return
+
+    sp.load_library()
+    w = workloads.get(args.config)
+    N, S, C = w.n_layers, w.n_steps, w.n_cells
+    K = args.steps if args.steps > 0 else S
+    timed_steps = [min(S - 1, int((i + 0.5) * S / K)) for i in range(K)]
+    warm_steps = [min(S - 1, int((i + 0.5) * S / max(1, args.warmup))) for i in range(args.warmup)]
+
+    log(f"workload {w.name}: N={N} C={C} Hq={w.n_q_heads} Hkv={w.n_kv_heads} D={w.head_dim} "
+        f"T_p={w.prompt_len} S={S}; timed steps K={K}")
+    t0 = time.time()
+    layers = [workloads.make_layer(w, l, device=dev) for l in range(N)]
+    qs = [workloads.make_q(w, l, 0, device=dev) for l in range(N)]
+    torch.cuda.synchronize()
+    log(f"inputs resident in HBM ({time.time() - t0:.1f} s, "
+        f"{torch.cuda.memory_allocated() / 2**30:.1f} GiB)")
+    shape = sp.make_shape(C, N, w.n_q_heads, w.n_kv_heads, w.head_dim, w.prompt_len, w.span, S,
+                          w.donor == "zero", w.dtype)
+    lw = workloads.cell_lw(w)
+    ws = sp.new_workspace(shape, device=dev)
+    out = torch.empty((C, w.n_q_heads, w.head_dim), dtype=torch.float32, device=dev)
+    lse = torch.empty((C, w.n_q_heads), dtype=torch.float32, device=dev)
+
+    def issue_step(s: int):
+        for l in range(N):
+            b = layers[l]
+            sp.splice_decode_attn(shape, sp.make_call(l, s, w.window(l), w.scale), lw, qs[l],
+                                  b["clean_k"], b["clean_v"], b["donor_k"], b["donor_v"],
+                                  b["gen_k"], b["gen_v"], out, lse, ws)
+
+    stream = torch.cuda.Stream(device=dev)
+    stream.wait_stream(torch.cuda.current_stream(dev))
+    graphs = {}
+    if not args.eager:
+        t0 = time.time()
+        for s in sorted(set(timed_steps) | set(warm_steps)):
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g, stream=stream):
+                issue_step(s)
+            graphs[s] = g
+        torch.cuda.synchronize()
+        log(f"captured {len(graphs)} step graphs of {N} launches ({time.time() - t0:.1f} s)")
+
+    def run(steps_list):
+        with torch.cuda.stream(stream):
+            for s in steps_list:
+                if args.eager:
+                    issue_step(s)
+                else:
+                    graphs[s].replay()
+
+    run(warm_steps)
+    torch.cuda.synchronize()
+    ev0 = torch.cuda.Event(enable_timing=True)
+    ev1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    ev0.record(stream)
+    run(timed_steps)
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    ms = ev0.elapsed_time(ev1)
+    sec = ms / 1e3
+    launches = K * N
+    alg_bytes = sum(call_bytes(w, l, s, spliced_flags(w, l, s)) for s in timed_steps for l in range(N))
+    gbs = alg_bytes / sec / 1e9
+    log(f"timed {launches} launches in {ms:.2f} ms: {gbs:.1f} GB/s algorithmic, "
+        f"{C * K / sec:.0f} cell-steps/s")
+
+    traffic, traffic_src = stored_traffic(w.name)
+    per_launch_bytes = alg_bytes / launches
+    avg_launch_s = sec / launches
+    roofline = {"bound": "hbm", "achieved": round(per_launch_bytes / avg_launch_s / 1e9, 2),
+                "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": round(per_launch_bytes / avg_launch_s / 1e9 / HBM_PEAK_GBS, 4),
+                "traffic": traffic, "kernel": "attn_kernel",
+                "bytes_per_launch": round(per_launch_bytes),
+                "avg_launch_us": round(avg_launch_s * 1e6, 3),
+                "traffic_source": traffic_src, "kernel_source_sha256_16": kernel_source_hash()}
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        log("timing the fp64 oracle on host cores (CPU baseline)")
+        cpu = cpu_baseline(w, args.cpu_seconds)
+        log(f"oracle: {cpu['value']} GB/s on {cpu['cores']} threads, {cpu['sample']}")
+
+    res = {
+        "metric": "spliced decode-attn HBM GB/s (% of peak) and sweep-cell decode steps/sec",
+        "value": round(gbs, 2), "unit": "GB/s", "n_gpus": 1, "steps": K, "warmup": args.warmup,
+        "ms_per_step": round(ms / K, 4), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": w.dtype, "data": "synthetic",
+        "pct_of_hbm_peak": round(100 * gbs / HBM_PEAK_GBS, 2),
+        "cell_steps_per_s": round(C * K / sec, 1),
+        "config": {"workload": w.name, "layers": N, "cells": C, "q_heads": w.n_q_heads,
+                   "kv_heads": w.n_kv_heads, "head_dim": w.head_dim, "prompt_len": w.prompt_len,
+                   "span": list(w.span), "decode_steps": S, "donor": w.donor,
+                   "launch": "eager" if args.eager else "hip-graph per decode step",
+                   "timed_steps": "evenly spaced over the sweep" if K != S else "full sweep"},
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,169 @@
+/*
+ * splice_attn.h -- C ABI of the MI355X (gfx950) spliced decode-attention library.
+ *
+ * The method (paper Section 3, "Splice intervention"; Algorithm 1 in the
+ * appendix "Splice Intervention Pseudocode"; donor forms in Table 1):
+ * a sweep cell (L, W) decodes greedily over a prefilled prompt cache of
+ * T_p slots per layer.  For every layer l >= L, from decode step W on, the
+ * prompt-span slots are read from a donor cache of the same length (or are
+ * all-zero for the ZERO donor) instead of the clean cache; generated entries
+ * are never modified.  Readings fixed by this ABI:
+ *   - step s is 0-based (s = 0 is the first decode pass after prefill) and
+ *     cell c is spliced at (layer, s) iff layer >= L_c and s >= W_c;
+ *   - only slots [span_lo, span_hi) are replaced ([0, T_p) is the
+ *     paper-literal whole-prompt splice);
+ *   - ZERO slots are keys with K = V = 0: they score exactly 0 and are not
+ *     masked, and the library never reads memory for them;
+ *   - the query of step s sits at position p = T_p + s and sees prompt slots
+ *     and generated rows 0..s; a window w > 0 keeps positions > p - w;
+ *   - q head h reads KV head floor(h / G) with G = n_q_heads / n_kv_heads.
+ * The library never copies a cache to splice it: each cell picks the clean
+ * or donor slot by pointer, so all cells of a call share one clean and one
+ * donor prompt cache.
+ *
+ * Memory and ownership.  Every tensor pointer is device memory owned by the
+ * caller; the library never allocates, frees or retains it.  Tensors are
+ * dense, row-major, 16-byte aligned:
+ *   q                        [C][Hq][D]                  dtype
+ *   clean_k, clean_v         [Hkv][T_p][D]               dtype
+ *   donor_k, donor_v         [Hkv][T_p][D]               dtype (NULL for ZERO)
+ *   gen_k, gen_v             [C][Hkv][gen_capacity][D]   dtype
+ *   out                      [C][Hq][D]                  fp32
+ *   lse                      [C][Hq]                     fp32, natural log
+ * cell_LW is HOST memory: int32 [C][2] = (L_c, W_c), read during the call.
+ * Work is enqueued on `stream` (a hipStream_t; NULL = the default stream)
+ * and runs asynchronously; the call returns once it is enqueued.
+ *
+ * Errors.  Arguments are validated on the host before anything is
+ * enqueued: on a negative status nothing was launched and no output byte
+ * was written.  SPLICE_EHIP reports a failed HIP launch.
+ * Calls are re-entrant (no global mutable state); two calls that share a
+ * workspace must be ordered on one stream.  Results are deterministic:
+ * identical inputs and the same split give identical bits.
+ */
+#ifndef SPLICE_ATTN_H
+#define SPLICE_ATTN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#if defined(__GNUC__)
+#define SPLICE_API __attribute__((visibility("default")))
+#else
+#define SPLICE_API
+#endif
+
+#define SPLICE_ABI_VERSION 1
+#define SPLICE_MAX_CELLS 256
+
+typedef enum {
+    SPLICE_OK = 0,
+    SPLICE_EINVAL = -1,        /* NULL pointer, bad enum value, misaligned pointer */
+    SPLICE_ESHAPE = -2,        /* sizes inconsistent with each other or with the call */
+    SPLICE_EWORKSPACE = -3,    /* workspace NULL or smaller than required */
+    SPLICE_EUNSUPPORTED = -4,  /* well-formed but not built: head_dim, group size, cells */
+    SPLICE_EHIP = -5           /* a HIP launch failed */
+} splice_status;
+
+typedef enum { SPLICE_DONOR_BUFFER = 0, SPLICE_DONOR_ZERO = 1 } splice_donor_kind;
+typedef enum { SPLICE_BF16 = 0, SPLICE_F32 = 1 } splice_dtype;
+typedef enum {
+    SPLICE_SRC_CLEAN = 0, SPLICE_SRC_DONOR = 1, SPLICE_SRC_ZERO = 2, SPLICE_SRC_GEN = 3
+} splice_src;
+
+typedef struct {
+    int32_t n_cells;       /* C, 0..SPLICE_MAX_CELLS (0: the call does nothing)        */
+    int32_t n_layers;      /* N > 0; layer must be < N                                */
+    int32_t n_q_heads;     /* Hq > 0                                                  */
+    int32_t n_kv_heads;    /* Hkv > 0, Hq % Hkv == 0, G = Hq / Hkv in {1, 2, 4, 8}     */
+    int32_t head_dim;      /* D in {64, 128, 256}                                     */
+    int32_t prompt_len;    /* T_p >= 0                                                */
+    int32_t span_lo;       /* 0 <= span_lo <= span_hi <= T_p                          */
+    int32_t span_hi;
+    int32_t gen_capacity;  /* rows per generated cache; step < gen_capacity           */
+    int32_t donor_kind;    /* splice_donor_kind                                       */
+    int32_t dtype;         /* splice_dtype of q and every K/V tensor                  */
+} splice_shape;
+
+typedef struct {
+    int32_t layer;         /* l, 0 <= l < N: enters only the splice predicate          */
+    int32_t step;          /* s, 0 <= s < gen_capacity: 0-based decode step            */
+    int32_t window;        /* sliding window w >= 0 (0: every key visible)            */
+    float scale;           /* softmax scale applied to q.k                            */
+    int32_t split_keys;    /* keys per work item, 0 = library default; else a
+                              multiple of 64 in [64, 65536] (tuning and tests)        */
+} splice_call;
+
+/* ABI version this library was built with (SPLICE_ABI_VERSION). */
+SPLICE_API int32_t splice_abi_version(void);
+
+/* Static string naming a status code; never NULL. */
+SPLICE_API const char *splice_status_str(int32_t status);
+
+/*
+ * Number of keys one query sees at `call`: visible prompt slots (all of
+ * them, spliced or not) plus visible generated rows.  The gather output of
+ * splice_kv_build has this many slots.  Negative splice_status on bad input.
+ */
+SPLICE_API int32_t splice_visible_len(const splice_shape *shape, const splice_call *call);
+
+/*
+ * Materialise what each cell attends to at `call` (Section 3, Algorithm 1):
+ *   out_k, out_v  device [C][Hkv][n_vis][D], dtype: slot t holds the t-th
+ *                 visible key/value -- prompt slots in position order
+ *                 (clean, donor or all-zero bits) then generated rows;
+ *   out_src       device uint8 [C][n_vis], a splice_src per slot.
+ * A bit-exact copy: it is the test hook for the splice selection and the
+ * copy-then-attend baseline that splice_decode_attn avoids.
+ */
+SPLICE_API int32_t splice_kv_build(const splice_shape *shape, const splice_call *call,
+                        const int32_t *cell_LW,
+                        const void *clean_k, const void *clean_v,
+                        const void *donor_k, const void *donor_v,
+                        const void *gen_k, const void *gen_v,
+                        void *out_k, void *out_v, uint8_t *out_src,
+                        void *stream);
+
+/*
+ * Workspace bytes splice_decode_attn needs for `call`.  With call == NULL:
+ * enough for every call on `shape` with split_keys == 0 (any layer, step,
+ * window).  Negative splice_status on bad input.
+ */
+SPLICE_API int64_t splice_decode_attn_workspace_bytes(const splice_shape *shape, const splice_call *call);
+
+/*
+ * Prepare a workspace once after allocating it: enqueues a fill kernel on
+ * `stream` (no memset node, so it may be graph-captured).  Every completed
+ * splice_decode_attn call leaves the workspace prepared again.
+ */
+SPLICE_API int32_t splice_workspace_init(void *workspace, size_t workspace_bytes, void *stream);
+
+/*
+ * Spliced single-query GQA decode attention for C sweep cells at one
+ * (layer, step) -- the attention read inside Algorithm 1's forward pass:
+ *   score_j = scale * q . k_j over each cell's visible keys,
+ *   out     = softmax(score) . V,     lse = log sum_j exp(score_j),
+ * with the keys and values chosen per cell as described at the top.
+ * q is read in dtype; accumulation is fp32; out and lse are fp32.
+ * `workspace` must hold splice_decode_attn_workspace_bytes(shape, call)
+ * bytes prepared by splice_workspace_init.
+ */
+SPLICE_API int32_t splice_decode_attn(const splice_shape *shape, const splice_call *call,
+                           const int32_t *cell_LW,
+                           const void *q,
+                           const void *clean_k, const void *clean_v,
+                           const void *donor_k, const void *donor_v,
+                           const void *gen_k, const void *gen_v,
+                           float *out, float *lse,
+                           void *workspace, size_t workspace_bytes,
+                           void *stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SPLICE_ATTN_H */

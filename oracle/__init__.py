@@ -17,7 +17,8 @@ from typing import Optional, Sequence, Tuple
 
 import numpy as np
 
-from .build import LIB, build
+from .build import LIB
+from .build import build as build_library
 
 _lib = None
 
@@ -41,7 +42,7 @@ def load(path: str = LIB):
     if _lib is not None and path == LIB:
         return _lib
     if not os.path.exists(path):
-        build()
+        build_library()
     lib = ctypes.CDLL(path)
     vp, i32p = ctypes.c_void_p, ctypes.POINTER(ctypes.c_int32)
     lib.oracle_spliced.argtypes = [ctypes.c_int] * 4

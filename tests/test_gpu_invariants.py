@@ -1,0 +1,148 @@
+"""Invariants of the method, reproduced by the GPU library itself:
+donor == clean and onsets past the step are bit-identical to unspliced, a
+cell's result does not depend on its batch-mates, repeat calls are
+bit-identical, and the split of the key list changes only rounding."""
+import numpy as np
+import pytest
+import torch
+
+import gpu_common as gc
+import oracle_pins
+import paper_2605_30574_amd as sp
+import workloads
+from workloads import DONOR_BLANK
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    sp.load_library()
+
+
+def _w():
+    return oracle_pins.tiny(dtype="bf16", donor=DONOR_BLANK, sink=True, n_steps=200).with_(
+        prompt_len=500, span=(40, 460), head_dim=128, scale=128 ** -0.5)
+
+
+@pytest.mark.parametrize("split", [0, 64])
+def test_donor_equal_clean_and_late_onset_are_unspliced(split):
+    w = _w()
+    lw = workloads.cell_lw(w)
+    never = np.array([[w.n_layers, 0]] * w.n_cells, dtype=np.int32)
+    for layer in range(w.n_layers):
+        bufs = gc.gpu_layer(w, layer)
+        same = dict(bufs, donor_k=bufs["clean_k"], donor_v=bufs["clean_v"])
+        for step in (0, 4, 199):
+            q = workloads.make_q(w, layer, step, device="cuda")
+            gc.announce(f"invariants layer={layer} step={step} split={split}")
+            o_u, l_u = gc.run_attn(w, layer, step, bufs, q, never, split=split)
+            o_s, l_s = gc.run_attn(w, layer, step, same, q, lw, split=split)
+            assert np.array_equal(o_u, o_s) and np.array_equal(l_u, l_s)
+            late = lw.copy()
+            late[:, 1] = step + 1
+            o_l, l_l = gc.run_attn(w, layer, step, bufs, q, late, split=split)
+            assert np.array_equal(o_u, o_l) and np.array_equal(l_u, l_l)
+
+
+def test_batch_independence_and_determinism():
+    w = _w()
+    lw = workloads.cell_lw(w)
+    layer, step = 1, 150
+    bufs = gc.gpu_layer(w, layer)
+    q = workloads.make_q(w, layer, step, device="cuda")
+    gc.announce("batch independence")
+    o_b, l_b = gc.run_attn(w, layer, step, bufs, q, lw, split=128)
+    o_r, l_r = gc.run_attn(w, layer, step, bufs, q, lw, split=128)
+    assert np.array_equal(o_b, o_r) and np.array_equal(l_b, l_r), "repeat call not bit-identical"
+    for c in range(w.n_cells):
+        one = dict(bufs, gen_k=bufs["gen_k"][c:c + 1].contiguous(), gen_v=bufs["gen_v"][c:c + 1].contiguous())
+        o1, l1 = gc.run_attn(w, layer, step, one, q[c:c + 1].contiguous(), lw[c:c + 1].copy(), split=128)
+        assert np.array_equal(o1[0], o_b[c]) and np.array_equal(l1[0], l_b[c]), f"cell {c}"
+    # reversed batch order
+    perm = np.arange(w.n_cells)[::-1].copy()
+    pb = dict(bufs, gen_k=bufs["gen_k"][perm].contiguous(), gen_v=bufs["gen_v"][perm].contiguous())
+    o_p, l_p = gc.run_attn(w, layer, step, pb, q[perm].contiguous(), lw[perm].copy(), split=128)
+    assert np.array_equal(o_p, o_b[perm]) and np.array_equal(l_p, l_b[perm])
+
+
+def test_split_changes_only_rounding():
+    w = _w()
+    lw = workloads.cell_lw(w)
+    layer, step = 0, 180
+    bufs = gc.gpu_layer(w, layer)
+    hb = gc.host(bufs)
+    q = workloads.make_q(w, layer, step, device="cuda")
+    ref_o, ref_l = gc.run_oracle(w, layer, step, hb, workloads.to_numpy(q), lw)
+    results = []
+    for split in (64, 128, 320, 704, 0):
+        gc.announce(f"split {split}")
+        o, l = gc.run_attn(w, layer, step, bufs, q, lw, split=split)
+        gc.assert_attn_close(o, l, ref_o, ref_l, f"split={split}")
+        results.append((o, l))
+    for o, l in results[1:]:
+        gc.assert_attn_close(o, l, results[0][0], results[0][1], "split vs split")
+
+
+def test_workspace_reuse_across_calls():
+    """One workspace serves a sequence of calls of different sizes; each
+    call leaves it ready for the next (the combine counters re-arm)."""
+    w = _w()
+    lw = workloads.cell_lw(w)
+    shape = gc.shape_of(w)
+    ws = sp.new_workspace(shape, sp.make_call(1, w.n_steps - 1, 0, w.scale, 64))
+    assert ws.numel() >= sp.splice_decode_attn_workspace_bytes(shape)
+    bufs = gc.gpu_layer(w, 1)
+    hb = gc.host(bufs)
+    for step in (199, 3, 120, 0, 199):
+        for split in (64, 0):
+            q = workloads.make_q(w, 1, step, device="cuda")
+            gc.announce(f"workspace reuse step={step} split={split}")
+            o, l = gc.run_attn(w, 1, step, bufs, q, lw, split=split, ws=ws)
+            ref_o, ref_l = gc.run_oracle(w, 1, step, hb, workloads.to_numpy(q), lw)
+            gc.assert_attn_close(o, l, ref_o, ref_l, f"reuse s={step} split={split}")
+
+
+def test_graph_replay_matches_eager():
+    """Calls captured in a HIP graph and replayed several times, with eager
+    work and synchronisation in between, give the eager bits every time."""
+    w = _w()
+    lw = workloads.cell_lw(w)
+    shape = gc.shape_of(w)
+    ws = sp.new_workspace(shape)
+    bufs = [gc.gpu_layer(w, layer) for layer in range(w.n_layers)]
+    steps = (0, 77, 199)
+    qs = {(l, s): workloads.make_q(w, l, s, device="cuda") for l in range(w.n_layers) for s in steps}
+    outs = {k: torch.empty((w.n_cells, w.n_q_heads, w.head_dim), device="cuda") for k in qs}
+    lses = {k: torch.empty((w.n_cells, w.n_q_heads), device="cuda") for k in qs}
+
+    def issue():
+        for (l, s) in qs:
+            b = bufs[l]
+            sp.splice_decode_attn(shape, sp.make_call(l, s, 0, w.scale), lw, qs[(l, s)], b["clean_k"],
+                                  b["clean_v"], b["donor_k"], b["donor_v"], b["gen_k"], b["gen_v"],
+                                  outs[(l, s)], lses[(l, s)], ws)
+
+    gc.announce("graph replay: eager reference")
+    issue()
+    torch.cuda.synchronize()
+    ref = {k: (outs[k].clone(), lses[k].clone()) for k in qs}
+    stream = torch.cuda.Stream()
+    stream.wait_stream(torch.cuda.current_stream())
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=stream):
+        issue()
+    torch.cuda.synchronize()
+    for rep in range(4):
+        for k in qs:
+            outs[k].fill_(float("nan"))
+            lses[k].fill_(float("nan"))
+        torch.cuda.synchronize()
+        gc.announce(f"graph replay {rep}")
+        g.replay()
+        torch.cuda.synchronize()
+        for k in qs:
+            assert torch.equal(outs[k], ref[k][0]) and torch.equal(lses[k], ref[k][1]), (rep, k)
+        issue()                                  # eager work between replays
+        torch.cuda.synchronize()

@@ -1,0 +1,177 @@
+"""GPU parity: the HIP library (through its C ABI) against the fp64 oracle on
+the same seeded inputs.  Gather and source map bit-exact; attention within
+max abs 1e-2 / mean abs 1e-3 on out and 1e-4 relative on lse."""
+import numpy as np
+import pytest
+import torch
+
+import gpu_common as gc
+import oracle_pins
+import paper_2605_30574_amd as sp
+import workloads
+from workloads import DONOR_BLANK, DONOR_DIFF, DONOR_ZERO
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    sp.load_library()
+
+
+def _check_call(w, layer, step, bufs, hb, lw, split=0, gather=True):
+    q = workloads.make_q(w, layer, step, device="cuda", n_cells=lw.shape[0])
+    gc.announce(f"{w.name} layer={layer} step={step} split={split} C={lw.shape[0]}")
+    out, lse = gc.run_attn(w, layer, step, bufs, q, lw, split=split)
+    ref_o, ref_l = gc.run_oracle(w, layer, step, hb, workloads.to_numpy(q), lw)
+    gc.assert_attn_close(out, lse, ref_o, ref_l, f"{w.name} l={layer} s={step} split={split}")
+    if gather:
+        ok, ov, src = gc.run_gather(w, layer, step, bufs, lw)
+        rk, rv, rs = gc.run_oracle_gather(w, layer, step, hb, lw)
+        assert np.array_equal(src, rs), f"source map {w.name} l={layer} s={step}"
+        assert np.array_equal(ok, rk), f"gathered K {w.name} l={layer} s={step}"
+        assert np.array_equal(ov, rv), f"gathered V {w.name} l={layer} s={step}"
+
+
+def test_tiny_sweep_every_call():
+    """The tiny fp32 ZERO sweep: every (layer, step), all 6 cells."""
+    w = workloads.get(0)
+    lw = workloads.cell_lw(w)
+    for layer in range(w.n_layers):
+        bufs = gc.gpu_layer(w, layer)
+        hb = gc.host(bufs)
+        for step in range(w.n_steps):
+            _check_call(w, layer, step, bufs, hb, lw)
+
+
+def _variant(name):
+    t = oracle_pins.tiny
+    return {
+        "bf16-blank-sink": t(dtype="bf16", donor=DONOR_BLANK, sink=True),
+        "bf16-diff": t(dtype="bf16", donor=DONOR_DIFF, sink=True),
+        "f32-window12": t(window=12),
+        "f32-fullspan-zero": t(span=(0, 32)),
+        "bf16-fullspan-blank": t(dtype="bf16", donor=DONOR_BLANK, span=(0, 32), sink=True),
+        "bf16-emptyspan": t(dtype="bf16", donor=DONOR_BLANK, span=(9, 9)),
+        "bf16-G1": t(dtype="bf16", donor=DONOR_BLANK).with_(n_q_heads=2, n_kv_heads=2),
+        "bf16-G8": t(dtype="bf16", donor=DONOR_ZERO).with_(n_q_heads=16, n_kv_heads=2),
+        "f32-G8-D256": t(donor=DONOR_BLANK).with_(n_q_heads=8, n_kv_heads=1, head_dim=256),
+        "bf16-D128": t(dtype="bf16", donor=DONOR_DIFF, sink=True).with_(head_dim=128, scale=128 ** -0.5),
+        "bf16-D256-window": t(dtype="bf16", donor=DONOR_BLANK, window=20, sink=True).with_(
+            head_dim=256, scale=1 / 16),
+        "bf16-long-blank": t(dtype="bf16", donor=DONOR_BLANK, sink=True, n_steps=300).with_(
+            prompt_len=700, span=(40, 660), head_dim=128, scale=128 ** -0.5),
+        "bf16-long-zero-window": t(dtype="bf16", donor=DONOR_ZERO, sink=True, n_steps=300,
+                                   window=600).with_(prompt_len=700, span=(40, 660), head_dim=128,
+                                                     scale=128 ** -0.5),
+    }[name]
+
+
+VARIANTS = ["bf16-blank-sink", "bf16-diff", "f32-window12", "f32-fullspan-zero", "bf16-fullspan-blank",
+            "bf16-emptyspan", "bf16-G1", "bf16-G8", "f32-G8-D256", "bf16-D128", "bf16-D256-window",
+            "bf16-long-blank", "bf16-long-zero-window"]
+
+
+@pytest.mark.parametrize("name", VARIANTS)
+def test_variant(name):
+    w = _variant(name)
+    lw = workloads.cell_lw(w)
+    S = w.n_steps
+    steps = sorted({0, 3, 4, 5, S // 2, S - 1})
+    for layer in range(w.n_layers):
+        bufs = gc.gpu_layer(w, layer)
+        hb = gc.host(bufs)
+        for step in steps:
+            for split in (0, 64):
+                _check_call(w, layer, step, bufs, hb, lw, split=split, gather=(split == 0))
+
+
+FULL = {1: (17, (0, 1, 8, 255, 511)), 2: (15, (0, 1, 64, 255)), 3: (5, (0, 1, 127)),
+        4: (20, (0, 2, 256, 1023))}
+
+
+@pytest.mark.parametrize("index", [1, 2, 3, 4])
+def test_full_size_sampled(index):
+    """Full-size caches of one layer, default split (the benchmark's launch),
+    every cell computed, sampled (cell, head) rows checked against the oracle;
+    the gather checked bit-exact on two cells."""
+    w = workloads.get(index)
+    layer, steps = FULL[index]
+    layers = (layer, 6) if index == 3 else (layer,)   # Gemma: a global and a local layer
+    lw = workloads.cell_lw(w)
+    C = w.n_cells
+    cells = sorted({0, 1, C // 3, C // 2, (2 * C) // 3, C - 2, C - 1})
+    rows = [(c, h) for c in cells for h in range(w.n_q_heads)]
+    for layer in layers:
+        gc.announce(f"{w.name}: building layer {layer} inputs")
+        bufs = gc.gpu_layer(w, layer)
+        hb = gc.host(bufs)
+        for step in steps:
+            q = workloads.make_q(w, layer, step, device="cuda")
+            gc.announce(f"{w.name} full-size layer={layer} step={step}")
+            out, lse = gc.run_attn(w, layer, step, bufs, q, lw)
+            assert np.all(np.isfinite(out)) and np.all(np.isfinite(lse))
+            ref_o, ref_l = gc.run_oracle(w, layer, step, hb, workloads.to_numpy(q), lw, rows=rows)
+            idx_c = np.array([r[0] for r in rows])
+            idx_h = np.array([r[1] for r in rows])
+            gc.assert_attn_close(out[idx_c, idx_h], lse[idx_c, idx_h], ref_o, ref_l,
+                                 f"{w.name} l={layer} s={step}")
+        # gather on a spliced and an unspliced cell
+        step = steps[-1]
+        pick = [c for c in range(C) if layer >= lw[c, 0]][:1] + [c for c in range(C) if layer < lw[c, 0]][:1]
+        sub_lw = np.ascontiguousarray(lw[pick])
+        sub = dict(bufs, gen_k=bufs["gen_k"][pick].contiguous(), gen_v=bufs["gen_v"][pick].contiguous())
+        hsub = dict(hb, gen_k=np.ascontiguousarray(hb["gen_k"][pick]), gen_v=np.ascontiguousarray(hb["gen_v"][pick]))
+        gc.announce(f"{w.name} full-size gather layer={layer} step={step} cells={pick}")
+        ok, ov, src = gc.run_gather(w, layer, step, sub, sub_lw)
+        rk, rv, rs = gc.run_oracle_gather(w, layer, step, hsub, sub_lw)
+        assert np.array_equal(src, rs) and np.array_equal(ok, rk) and np.array_equal(ov, rv)
+        del bufs, hb
+        torch.cuda.empty_cache()
+
+
+def test_edge_no_prompt_and_windows():
+    base = oracle_pins.tiny(dtype="bf16", donor=DONOR_BLANK).with_(prompt_len=0, span=(0, 0))
+    lw = workloads.cell_lw(base)
+    bufs = gc.gpu_layer(base, 0)
+    hb = gc.host(bufs)
+    for step in (0, 7, 15):
+        _check_call(base, 0, step, bufs, hb, lw)
+    # window 1: only the query's own generated row is visible
+    w1 = oracle_pins.tiny(dtype="bf16", donor=DONOR_BLANK, window=1)
+    bufs = gc.gpu_layer(w1, 1)
+    hb = gc.host(bufs)
+    for step in (0, 5, 15):
+        _check_call(w1, 1, step, bufs, hb, workloads.cell_lw(w1))
+
+
+def test_edge_max_cells_and_single_cell():
+    w = oracle_pins.tiny(dtype="bf16", donor=DONOR_BLANK).with_(
+        n_q_heads=2, n_kv_heads=1, prompt_len=16, span=(2, 14), n_steps=4,
+        cells=tuple((L, W) for L in range(64) for W in range(4)))
+    assert w.n_cells == sp.SPLICE_MAX_CELLS
+    w = w.with_(n_layers=64)
+    lw = workloads.cell_lw(w)
+    bufs = gc.gpu_layer(w, 30)
+    hb = gc.host(bufs)
+    for step in (0, 3):
+        _check_call(w, 30, step, bufs, hb, lw)
+    one = w.with_(cells=((10, 1),))
+    b1 = gc.gpu_layer(one, 30)
+    _check_call(one, 30, 2, b1, gc.host(b1), workloads.cell_lw(one))
+
+
+def test_zero_cells_is_a_noop():
+    w = workloads.get(0)
+    shape = gc.shape_of(w, n_cells=0)
+    call = sp.make_call(0, 0, 0, w.scale)
+    out = torch.full((1,), 7.0, device="cuda")
+    lse = torch.full((1,), 7.0, device="cuda")
+    lib = sp.load_library()
+    import ctypes
+    rc = lib.splice_decode_attn(ctypes.byref(shape), ctypes.byref(call), None, *([None] * 8),
+                                ctypes.c_void_p(out.data_ptr()), ctypes.c_void_p(lse.data_ptr()),
+                                None, 0, None)
+    torch.cuda.synchronize()
+    assert rc == sp.SPLICE_OK and out.item() == 7.0 and lse.item() == 7.0
