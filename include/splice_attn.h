@@ -25,8 +25,9 @@
  * caller; the library never allocates, frees or retains it.  Tensors are
  * dense, row-major, 16-byte aligned:
  *   q                        [C][Hq][D]                  dtype
- *   clean_k, clean_v         [Hkv][T_p][D]               dtype
- *   donor_k, donor_v         [Hkv][T_p][D]               dtype (NULL for ZERO)
+ *   clean_k, clean_v         [Hkv][T_p][D]               dtype (may be NULL if T_p == 0)
+ *   donor_k, donor_v         [Hkv][T_p][D]               dtype (NULL for ZERO;
+ *                                                        may be NULL if T_p == 0)
  *   gen_k, gen_v             [C][Hkv][gen_capacity][D]   dtype
  *   out                      [C][Hq][D]                  fp32
  *   lse                      [C][Hq]                     fp32, natural log
@@ -136,9 +137,11 @@ SPLICE_API int32_t splice_kv_build(const splice_shape *shape, const splice_call 
 SPLICE_API int64_t splice_decode_attn_workspace_bytes(const splice_shape *shape, const splice_call *call);
 
 /*
- * Prepare a workspace once after allocating it: enqueues a fill kernel on
- * `stream` (no memset node, so it may be graph-captured).  Every completed
- * splice_decode_attn call leaves the workspace prepared again.
+ * Zero a workspace with a fill kernel enqueued on `stream` (no memset node,
+ * so it may be graph-captured).  splice_decode_attn does not depend on the
+ * workspace's prior contents -- it writes every partial-result slot before a
+ * second kernel of the same call reads it -- so this is optional hygiene.
+ * workspace must be 256-byte aligned and workspace_bytes a multiple of 4.
  */
 SPLICE_API int32_t splice_workspace_init(void *workspace, size_t workspace_bytes, void *stream);
 
@@ -149,8 +152,10 @@ SPLICE_API int32_t splice_workspace_init(void *workspace, size_t workspace_bytes
  *   out     = softmax(score) . V,     lse = log sum_j exp(score_j),
  * with the keys and values chosen per cell as described at the top.
  * q is read in dtype; accumulation is fp32; out and lse are fp32.
- * `workspace` must hold splice_decode_attn_workspace_bytes(shape, call)
- * bytes prepared by splice_workspace_init.
+ * `workspace` (256-byte aligned) must hold
+ * splice_decode_attn_workspace_bytes(shape, call) bytes; it holds the
+ * split-K partial results between the call's two kernels, so calls that
+ * share a workspace must be ordered on one stream.
  */
 SPLICE_API int32_t splice_decode_attn(const splice_shape *shape, const splice_call *call,
                            const int32_t *cell_LW,

@@ -118,21 +118,20 @@ inline int ceil_div(int64_t a, int64_t b) { return (int)((a + b - 1) / b); }
 inline int slot_floats(int G, int D) { return (G * D + 2 * G + 63) / 64 * 64; }
 
 struct WorkspaceLayout {
-    size_t counters_off, counters_bytes;
     size_t part_off, part_bytes;
     size_t total;
 };
 
+// The workspace holds one partial-result slot per (cell, KV head, chunk).
 inline WorkspaceLayout workspace_layout(const splice_shape &sh, int max_chunks) {
     WorkspaceLayout w;
     const int64_t pairs = (int64_t)sh.n_cells * sh.n_kv_heads;
-    w.counters_off = 0;
-    w.counters_bytes = (size_t)((pairs * 4 + 255) / 256 * 256);
-    w.part_off = w.counters_bytes;
-    w.part_bytes = (size_t)pairs * (size_t)max_chunks *
-                   (size_t)slot_floats(group_of(sh), sh.head_dim) * sizeof(float);
+    w.part_off = 0;
+    w.part_bytes = max_chunks > 1 ? (size_t)pairs * (size_t)max_chunks *
+                                        (size_t)slot_floats(group_of(sh), sh.head_dim) * sizeof(float)
+                                  : 0;
     w.total = w.part_off + w.part_bytes;
-    if (w.total == 0) w.total = 256;
+    if (w.total < 256) w.total = 256;
     return w;
 }
 

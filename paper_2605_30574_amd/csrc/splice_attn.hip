@@ -16,12 +16,16 @@
 //                   the row group; every row group keeps its own online
 //                   softmax state (max, sum, weighted V) for the G query
 //                   heads of the KV head.  States merge across row groups
-//                   (lane shuffles) and waves (LDS) into one partial per
-//                   work item.  The last work item of a (cell, KV head) to
-//                   finish -- found with a device-scope counter -- merges
-//                   the partials (log-sum-exp combine), adds the ZERO donor's
-//                   closed-form term and writes out/lse, then re-arms the
-//                   counter.  One launch per call.
+//                   (lane shuffles) and waves (LDS).  A cell whose list fits
+//                   one chunk is finished here; otherwise the item writes a
+//                   partial (m, l, o) to the workspace.
+//   combine_kernel  merges the partials of each (cell, KV head) with a
+//                   log-sum-exp combine in chunk order, adds the ZERO
+//                   donor's closed-form term and writes out/lse.  It is a
+//                   separate launch: the kernel boundary makes the partials
+//                   visible across XCDs without device-scope fences, whose
+//                   L2 write-back and invalidate cost every other work item
+//                   its cached prompt tiles.
 //   fill_kernel     splice_workspace_init.
 //
 // ZERO donor: a ZERO slot has K = V = 0, so its score is exactly 0 and it
@@ -69,6 +73,9 @@ __device__ __forceinline__ float group_sum(float x) {
         x += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(x), 0x140, 0xF, 0xF, false));
     return x;
 }
+
+// 2^x with v_exp_f32 (results below 2^-126 flush to zero: negligible weights).
+__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
 __device__ __forceinline__ bool bit_set(const uint32_t *mask, int c) {
     return (mask[c >> 5] >> (c & 31)) & 1u;
@@ -133,7 +140,6 @@ struct AttnArgs {
     const char *ck, *cv, *dk, *dv, *gk, *gv;
     float *out, *lse;
     float *part;
-    int *counters;
     int Hq, Hkv, Tp, cap, step;
     int jp0, i0, sa, sb, n_gen;
     int zero_donor;
@@ -141,6 +147,13 @@ struct AttnArgs {
     float qk_scale;   // scale * log2(e)
     uint32_t spliced[SPLICE_MAX_CELLS / 32];
 };
+
+// Length of cell c's key list: visible prompt slots (without the ZERO slots of
+// a spliced cell, which never enter the list) plus visible generated rows.
+__device__ __forceinline__ int list_len(const AttnArgs &a, int c) {
+    const bool zskip = a.zero_donor && bit_set(a.spliced, c);
+    return (a.Tp - a.jp0) - (zskip ? a.sb - a.sa : 0) + a.n_gen;
+}
 
 // Lane layout for one K/V row of D elements (EB bytes each):
 //   LPK = D / 16 lanes per row ("row group"), KPW = 64 / LPK rows per wave;
@@ -162,7 +175,6 @@ __global__ __launch_bounds__(kThreads) void attn_kernel(AttnArgs a) {
     __shared__ float s_o[kWaves][G][D];
     __shared__ float s_m[kWaves][G];
     __shared__ float s_l[kWaves][G];
-    __shared__ int s_last;
 
     const int tid = threadIdx.x;
     const int lane = tid & 63, wave = tid >> 6;
@@ -291,14 +303,14 @@ __global__ __launch_bounds__(kThreads) void attn_kernel(AttnArgs a) {
 #pragma unroll
             for (int u = 0; u < U; ++u) mx = fmaxf(mx, s[u][h]);
             const float ms = mx == -INFINITY ? 0.f : mx;
-            const float alpha = exp2f(m[h] - ms);
+            const float alpha = fast_exp2(m[h] - ms);
             l[h] *= alpha;
 #pragma unroll
             for (int e = 0; e < 16; ++e) o[h][e] *= alpha;
             m[h] = mx;
 #pragma unroll
             for (int u = 0; u < U; ++u) {
-                const float pw = exp2f(s[u][h] - ms);
+                const float pw = fast_exp2(s[u][h] - ms);
                 l[h] += pw;
 #pragma unroll
                 for (int e = 0; e < 16; ++e) o[h][e] = fmaf(pw, vf[u][e], o[h][e]);
@@ -315,7 +327,7 @@ __global__ __launch_bounds__(kThreads) void attn_kernel(AttnArgs a) {
             const float lo = __shfl_xor(l[h], off);
             const float mx = fmaxf(m[h], mo);
             const float ms = mx == -INFINITY ? 0.f : mx;
-            const float fa = exp2f(m[h] - ms), fb = exp2f(mo - ms);
+            const float fa = fast_exp2(m[h] - ms), fb = fast_exp2(mo - ms);
             l[h] = l[h] * fa + lo * fb;
 #pragma unroll
             for (int e = 0; e < 16; ++e) {
@@ -355,15 +367,15 @@ __global__ __launch_bounds__(kThreads) void attn_kernel(AttnArgs a) {
         float L = 0.f, O = 0.f;
 #pragma unroll
         for (int w = 0; w < kWaves; ++w) {
-            const float f = exp2f(s_m[w][h] - Ms);
+            const float f = fast_exp2(s_m[w][h] - Ms);
             L = fmaf(s_l[w][h], f, L);
             O = fmaf(s_o[w][h][d], f, O);
         }
         if (n_chunks == 1) {
             if (zero_term) {
                 const float Mz = fmaxf(M, 0.f);
-                const float f = exp2f(M - Mz);
-                L = L * f + (float)nsv * exp2f(-Mz);
+                const float f = fast_exp2(M - Mz);
+                L = L * f + (float)nsv * fast_exp2(-Mz);
                 O *= f;
                 M = Mz;
             }
@@ -378,36 +390,35 @@ __global__ __launch_bounds__(kThreads) void attn_kernel(AttnArgs a) {
             }
         }
     }
-    if (n_chunks == 1) return;
+}
 
-    // last-arriving work item of this (cell, KV head) combines the partials
-    __threadfence();
-    __syncthreads();
-    if (tid == 0) {
-        const int prev = atomicAdd(&a.counters[c * a.Hkv + g], 1);
-        s_last = (prev == n_chunks - 1);
-    }
-    __syncthreads();
-    if (!s_last) return;
-    __threadfence();
-
-    for (int e = tid; e < G * D; e += kThreads) {
+// Merge the partials of one (cell, KV head) in chunk order (grid: C * Hkv).
+template <int D, int G>
+__global__ __launch_bounds__(kThreads) void combine_kernel(AttnArgs a) {
+    const int g = blockIdx.x % a.Hkv;
+    const int c = blockIdx.x / a.Hkv;
+    const int n_chunks = (list_len(a, c) + a.split - 1) / a.split;
+    if (n_chunks <= 1) return;   // finished by the attention kernel
+    const bool zero_term = a.zero_donor && bit_set(a.spliced, c) && a.sb > a.sa;
+    const float nsv = (float)(a.sb - a.sa);
+    const float *slot_base = a.part + ((size_t)(c * a.Hkv + g) * a.max_chunks) * a.slot_floats;
+    const int row0 = c * a.Hq + g * G;
+    for (int e = threadIdx.x; e < G * D; e += kThreads) {
         const int h = e / D, d = e % D;
         float M = zero_term ? 0.f : -INFINITY;
         for (int k = 0; k < n_chunks; ++k)
             M = fmaxf(M, slot_base[(size_t)k * a.slot_floats + G * D + h]);
-        float L = zero_term ? (float)nsv * exp2f(-M) : 0.f;
+        float L = zero_term ? nsv * fast_exp2(-M) : 0.f;
         float O = 0.f;
         for (int k = 0; k < n_chunks; ++k) {
             const float *slot = slot_base + (size_t)k * a.slot_floats;
-            const float f = exp2f(slot[G * D + h] - M);
+            const float f = fast_exp2(slot[G * D + h] - M);
             L = fmaf(slot[G * D + G + h], f, L);
             O = fmaf(slot[h * D + d], f, O);
         }
         a.out[(size_t)(row0 + h) * D + d] = O / L;
         if (d == 0) a.lse[row0 + h] = (M + log2f(L)) * kLn2;
     }
-    if (tid == 0) atomicExch(&a.counters[c * a.Hkv + g], 0);
 }
 
 __global__ __launch_bounds__(kThreads) void fill_kernel(uint32_t *p, size_t n_words) {
@@ -419,29 +430,37 @@ __global__ __launch_bounds__(kThreads) void fill_kernel(uint32_t *p, size_t n_wo
 // ------------------------------------------------------------ dispatch
 
 typedef void (*attn_fn)(AttnArgs);
+struct AttnKernels {
+    attn_fn attn, combine;
+};
+
+template <int D, int G, bool BF16>
+AttnKernels kernels_of() {
+    return AttnKernels{attn_kernel<D, G, BF16>, combine_kernel<D, G>};
+}
 
 template <int D, bool BF16>
-attn_fn pick_g(int G) {
+AttnKernels pick_g(int G) {
     switch (G) {
-    case 1: return attn_kernel<D, 1, BF16>;
-    case 2: return attn_kernel<D, 2, BF16>;
-    case 4: return attn_kernel<D, 4, BF16>;
-    case 8: return attn_kernel<D, 8, BF16>;
-    default: return nullptr;
+    case 1: return kernels_of<D, 1, BF16>();
+    case 2: return kernels_of<D, 2, BF16>();
+    case 4: return kernels_of<D, 4, BF16>();
+    case 8: return kernels_of<D, 8, BF16>();
+    default: return AttnKernels{nullptr, nullptr};
     }
 }
 
 template <bool BF16>
-attn_fn pick_d(int D, int G) {
+AttnKernels pick_d(int D, int G) {
     switch (D) {
     case 64: return pick_g<64, BF16>(G);
     case 128: return pick_g<128, BF16>(G);
     case 256: return pick_g<256, BF16>(G);
-    default: return nullptr;
+    default: return AttnKernels{nullptr, nullptr};
     }
 }
 
-attn_fn pick_attn(int D, int G, int dtype) {
+AttnKernels pick_attn(int D, int G, int dtype) {
     return dtype == SPLICE_BF16 ? pick_d<true>(D, G) : pick_d<false>(D, G);
 }
 
@@ -503,8 +522,10 @@ int32_t splice_kv_build(const splice_shape *shape, const splice_call *call, cons
     if (rc != SPLICE_OK) return rc;
     if (sh.n_cells == 0) return SPLICE_OK;
     const bool zero = sh.donor_kind == SPLICE_DONOR_ZERO;
-    if (!clean_k || !clean_v || !gen_k || !gen_v || !out_k || !out_v || !out_src) return SPLICE_EINVAL;
-    if (zero ? (donor_k || donor_v) : (!donor_k || !donor_v)) return SPLICE_EINVAL;
+    const bool has_prompt = sh.prompt_len > 0;   // an empty prompt has no prompt buffers to read
+    if (!gen_k || !gen_v || !out_k || !out_v || !out_src) return SPLICE_EINVAL;
+    if (has_prompt && (!clean_k || !clean_v)) return SPLICE_EINVAL;
+    if (zero ? (donor_k || donor_v) : (has_prompt && (!donor_k || !donor_v))) return SPLICE_EINVAL;
     const void *ptrs[] = {clean_k, clean_v, gen_k, gen_v, out_k, out_v};
     for (const void *p : ptrs)
         if (!splice::aligned(p, 16)) return SPLICE_EINVAL;
@@ -570,8 +591,10 @@ int32_t splice_decode_attn(const splice_shape *shape, const splice_call *call, c
     if (rc != SPLICE_OK) return rc;
     if (sh.n_cells == 0) return SPLICE_OK;
     const bool zero = sh.donor_kind == SPLICE_DONOR_ZERO;
-    if (!q || !clean_k || !clean_v || !gen_k || !gen_v || !out || !lse) return SPLICE_EINVAL;
-    if (zero ? (donor_k || donor_v) : (!donor_k || !donor_v)) return SPLICE_EINVAL;
+    const bool has_prompt = sh.prompt_len > 0;   // an empty prompt has no prompt buffers to read
+    if (!q || !gen_k || !gen_v || !out || !lse) return SPLICE_EINVAL;
+    if (has_prompt && (!clean_k || !clean_v)) return SPLICE_EINVAL;
+    if (zero ? (donor_k || donor_v) : (has_prompt && (!donor_k || !donor_v))) return SPLICE_EINVAL;
     const void *ptrs[] = {q, clean_k, clean_v, gen_k, gen_v};
     for (const void *p : ptrs)
         if (!splice::aligned(p, 16)) return SPLICE_EINVAL;
@@ -586,8 +609,8 @@ int32_t splice_decode_attn(const splice_shape *shape, const splice_call *call, c
     if (workspace_bytes < wl.total) return SPLICE_EWORKSPACE;
 
     const int G = splice::group_of(sh);
-    attn_fn fn = pick_attn(sh.head_dim, G, sh.dtype);
-    if (!fn) return SPLICE_EUNSUPPORTED;
+    const AttnKernels kern = pick_attn(sh.head_dim, G, sh.dtype);
+    if (!kern.attn) return SPLICE_EUNSUPPORTED;
 
     AttnArgs a;
     a.q = q;
@@ -595,7 +618,6 @@ int32_t splice_decode_attn(const splice_shape *shape, const splice_call *call, c
     a.dk = (const char *)donor_k; a.dv = (const char *)donor_v;
     a.gk = (const char *)gen_k; a.gv = (const char *)gen_v;
     a.out = out; a.lse = lse;
-    a.counters = (int *)((char *)workspace + wl.counters_off);
     a.part = (float *)((char *)workspace + wl.part_off);
     a.Hq = sh.n_q_heads; a.Hkv = sh.n_kv_heads; a.Tp = sh.prompt_len; a.cap = sh.gen_capacity;
     a.step = call->step;
@@ -609,7 +631,10 @@ int32_t splice_decode_attn(const splice_shape *shape, const splice_call *call, c
 
     const int64_t items = (int64_t)sh.n_cells * sh.n_kv_heads * max_chunks;
     if (items > INT32_MAX) return SPLICE_EUNSUPPORTED;
-    hipLaunchKernelGGL(fn, dim3((unsigned)items), dim3(kThreads), 0, (hipStream_t)stream, a);
+    hipLaunchKernelGGL(kern.attn, dim3((unsigned)items), dim3(kThreads), 0, (hipStream_t)stream, a);
+    if (max_chunks > 1)
+        hipLaunchKernelGGL(kern.combine, dim3((unsigned)(sh.n_cells * sh.n_kv_heads)), dim3(kThreads), 0,
+                           (hipStream_t)stream, a);
     return launch_status();
 }
 

@@ -126,6 +126,8 @@ def _dev_ptr(t, name: str, numel: int, dtype, device=None, optional: bool = Fals
         if optional:
             return None, device
         raise ValueError(f"{name} is required")
+    if numel == 0 and t.numel() == 0:
+        return None, (t.device if device is None else device)   # empty buffer: NULL
     if not t.is_cuda:
         raise ValueError(f"{name} must be a GPU tensor")
     if dtype is not None and t.dtype != dtype:

@@ -87,7 +87,7 @@ def test_split_changes_only_rounding():
 
 def test_workspace_reuse_across_calls():
     """One workspace serves a sequence of calls of different sizes; each
-    call leaves it ready for the next (the combine counters re-arm)."""
+    call writes every partial slot it reads, so stale contents never leak."""
     w = _w()
     lw = workloads.cell_lw(w)
     shape = gc.shape_of(w)

@@ -160,18 +160,3 @@ def test_edge_max_cells_and_single_cell():
     one = w.with_(cells=((10, 1),))
     b1 = gc.gpu_layer(one, 30)
     _check_call(one, 30, 2, b1, gc.host(b1), workloads.cell_lw(one))
-
-
-def test_zero_cells_is_a_noop():
-    w = workloads.get(0)
-    shape = gc.shape_of(w, n_cells=0)
-    call = sp.make_call(0, 0, 0, w.scale)
-    out = torch.full((1,), 7.0, device="cuda")
-    lse = torch.full((1,), 7.0, device="cuda")
-    lib = sp.load_library()
-    import ctypes
-    rc = lib.splice_decode_attn(ctypes.byref(shape), ctypes.byref(call), None, *([None] * 8),
-                                ctypes.c_void_p(out.data_ptr()), ctypes.c_void_p(lse.data_ptr()),
-                                None, 0, None)
-    torch.cuda.synchronize()
-    assert rc == sp.SPLICE_OK and out.item() == 7.0 and lse.item() == 7.0
