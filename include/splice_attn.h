@@ -23,7 +23,7 @@
  *
  * Memory and ownership.  Every tensor pointer is device memory owned by the
  * caller; the library never allocates, frees or retains it.  Tensors are
- * dense, row-major, 16-byte aligned:
+ * dense, row-major, 16-byte aligned (lse: 4-byte aligned):
  *   q                        [C][Hq][D]                  dtype
  *   clean_k, clean_v         [Hkv][T_p][D]               dtype (may be NULL if T_p == 0)
  *   donor_k, donor_v         [Hkv][T_p][D]               dtype (NULL for ZERO;

@@ -98,56 +98,122 @@ inline bool cell_spliced(const int32_t *cell_LW, int c, int layer, int step) {
 }
 
 // ---------------------------------------------------------------- attention plan
+//
+// One call = one launch of prompt work items and generated-span work items.
+//   prompt items (bf16): (KV head, block of kRowBlock rows, prompt chunk); the
+//     rows of a KV head are the (cell, q head) pairs of every cell, clean
+//     cells first, so one staged K/V tile serves kRowBlock rows;
+//   prompt items (f32):  (cell, KV head, prompt chunk), on the vector ALUs;
+//   generated items:     (cell, KV head, chunk of the generated rows).
+// Every (cell, KV head) receives one partial result per prompt chunk and per
+// generated chunk; the last of them to finish merges them.
 
-constexpr int kTargetItems = 2048;   // work items a default split aims for
-constexpr int kMinSplit = 256;       // default split never goes below this
-constexpr int kMaxSplit = 2048;      // ... nor above this
-
-inline int default_split(int n_keys, int n_cells, int n_kv_heads) {
-    const int64_t pairs = (int64_t)n_cells * n_kv_heads;
-    int64_t want = ((int64_t)n_keys * pairs + kTargetItems - 1) / kTargetItems;   // ceil
-    want = (want + 63) / 64 * 64;
-    if (want < kMinSplit) want = kMinSplit;
-    if (want > kMaxSplit) want = kMaxSplit;
-    return (int)want;
-}
+constexpr int kRowBlock = 64;              // rows per bf16 prompt item
+constexpr int kMinChunk = 256;             // a default chunk is at least this long
+constexpr int kMaxChunks = 32;             // default chunks per part (prompt, generated)
+constexpr int kMaxSlots = 64;              // partial results per (cell, KV head)
+constexpr int kPromptItemsTarget = 512;    // prompt items a default split aims for
+constexpr int kGenItemsTarget = 2048;      // generated items a default split aims for
 
 inline int ceil_div(int64_t a, int64_t b) { return (int)((a + b - 1) / b); }
+inline int round_up(int64_t a, int64_t m) { return (int)((a + m - 1) / m * m); }
 
 // Floats per partial-result slot: o[G][D], m[G], l[G], padded to 256 bytes.
 inline int slot_floats(int G, int D) { return (G * D + 2 * G + 63) / 64 * 64; }
 
+inline bool mfma_prompt(const splice_shape &sh) { return sh.dtype == SPLICE_BF16; }
+
+inline int row_blocks(const splice_shape &sh) {
+    return ceil_div((int64_t)sh.n_cells * group_of(sh), kRowBlock);
+}
+
+// Prompt items per prompt chunk.
+inline int prompt_items_per_chunk(const splice_shape &sh) {
+    return sh.n_kv_heads * (mfma_prompt(sh) ? row_blocks(sh) : sh.n_cells);
+}
+
+inline int prompt_chunk_target(const splice_shape &sh) {
+    const int per = prompt_items_per_chunk(sh);
+    const int t = per > 0 ? kPromptItemsTarget / per : 1;
+    return t < 1 ? 1 : (t > kMaxChunks ? kMaxChunks : t);
+}
+
+inline int gen_chunk_target(const splice_shape &sh) {
+    const int64_t pairs = (int64_t)sh.n_cells * sh.n_kv_heads;
+    const int64_t t = pairs > 0 ? kGenItemsTarget / pairs : 1;
+    return t < 1 ? 1 : (t > kMaxChunks ? kMaxChunks : (int)t);
+}
+
+// Cut n keys into chunks.  Default: k = min(ceil(n / kMinChunk), target)
+// chunks of equal length rounded up to 64; split > 0 fixes the length.
+inline void cut(int n, int target, int split, int *k, int *len) {
+    if (n <= 0) {
+        *k = 0;
+        *len = 64;
+        return;
+    }
+    if (split > 0) {
+        *len = split;
+        *k = ceil_div(n, split);
+        return;
+    }
+    int kk = ceil_div(n, kMinChunk);
+    if (kk > target) kk = target;
+    *len = round_up(ceil_div(n, kk), 64);
+    *k = ceil_div(n, *len);
+}
+
+struct AttnPlan {
+    Geometry geo;
+    int n_p, p_len;          // prompt chunks over the visible prompt
+    int n_g, g_len;          // chunks over the visible generated rows
+    int n_slots;             // n_p + n_g partial results per (cell, KV head)
+    int n_prompt_items, n_gen_items;
+};
+
+inline AttnPlan plan_attn(const splice_shape &sh, const splice_call &call) {
+    AttnPlan p;
+    p.geo = geometry(sh, call);
+    cut(p.geo.n_prompt, prompt_chunk_target(sh), call.split_keys, &p.n_p, &p.p_len);
+    cut(p.geo.n_gen, gen_chunk_target(sh), call.split_keys, &p.n_g, &p.g_len);
+    p.n_slots = p.n_p + p.n_g;
+    p.n_prompt_items = prompt_items_per_chunk(sh) * p.n_p;
+    p.n_gen_items = sh.n_cells * sh.n_kv_heads * p.n_g;
+    return p;
+}
+
 struct WorkspaceLayout {
+    size_t counters_off, counters_bytes;
     size_t part_off, part_bytes;
     size_t total;
 };
 
-// The workspace holds one partial-result slot per (cell, KV head, chunk).
-inline WorkspaceLayout workspace_layout(const splice_shape &sh, int max_chunks) {
+// Counters [C][Hkv] (int32), then one partial slot per (cell, KV head, chunk).
+inline WorkspaceLayout workspace_layout(const splice_shape &sh, int n_slots) {
     WorkspaceLayout w;
     const int64_t pairs = (int64_t)sh.n_cells * sh.n_kv_heads;
-    w.part_off = 0;
-    w.part_bytes = max_chunks > 1 ? (size_t)pairs * (size_t)max_chunks *
-                                        (size_t)slot_floats(group_of(sh), sh.head_dim) * sizeof(float)
-                                  : 0;
+    w.counters_off = 0;
+    w.counters_bytes = (size_t)round_up(pairs * 4, 256);
+    w.part_off = w.counters_bytes;
+    w.part_bytes = (size_t)pairs * (size_t)n_slots * (size_t)slot_floats(group_of(sh), sh.head_dim) * 4;
     w.total = w.part_off + w.part_bytes;
     if (w.total < 256) w.total = 256;
     return w;
 }
 
-// Largest number of work items per (cell, KV head) of any default-split call
-// on this shape.  A call has n <= T_p + gen_capacity keys and split(n) is
-// either >= n * pairs / kTargetItems (so n / split <= kTargetItems / pairs)
-// or clamped to kMaxSplit (so n / split <= (T_p + gen_capacity) / kMaxSplit).
-inline int worst_default_chunks(const splice_shape &sh) {
-    const int64_t pairs = (int64_t)sh.n_cells * sh.n_kv_heads;
-    if (pairs <= 0) return 1;
-    const int64_t n_max = (int64_t)sh.prompt_len + sh.gen_capacity;
-    const int a = ceil_div(kTargetItems, pairs);
-    const int b = ceil_div(n_max, kMaxSplit);
-    const int worst = a > b ? a : b;
-    const int cap = ceil_div(n_max, kMinSplit);   // split >= kMinSplit always
-    return worst < cap ? worst : cap;
+// Most slots any default-split call on this shape uses.  For n keys the
+// default cut makes at most min(ceil(n / kMinChunk), target) chunks (each
+// chunk is at least n / that many keys long), and that bound grows with n;
+// a call sees at most T_p prompt keys and gen_capacity generated rows.
+inline int max_default_chunks(int n, int target) {
+    if (n <= 0) return 0;
+    const int k = ceil_div(n, kMinChunk);
+    return k < target ? k : target;
+}
+
+inline int worst_default_slots(const splice_shape &sh) {
+    return max_default_chunks(sh.prompt_len, prompt_chunk_target(sh)) +
+           max_default_chunks(sh.gen_capacity, gen_chunk_target(sh));
 }
 
 }  // namespace splice

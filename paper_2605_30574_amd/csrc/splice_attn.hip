@@ -9,23 +9,23 @@
 // Kernels
 //   gather_kernel   splice_kv_build: bit-exact copy of each cell's visible
 //                   keys/values plus a source code per slot (16-byte moves).
-//   attn_kernel     splice_decode_attn: one work item = (cell, KV head,
-//                   chunk of the cell's key list).  Lanes stream K/V rows
-//                   from HBM with coalesced 16-byte loads, D/16 lanes per
-//                   row; q.k uses v_dot2_f32_bf16 and a DPP butterfly inside
-//                   the row group; every row group keeps its own online
-//                   softmax state (max, sum, weighted V) for the G query
-//                   heads of the KV head.  States merge across row groups
-//                   (lane shuffles) and waves (LDS).  A cell whose list fits
-//                   one chunk is finished here; otherwise the item writes a
-//                   partial (m, l, o) to the workspace.
-//   combine_kernel  merges the partials of each (cell, KV head) with a
-//                   log-sum-exp combine in chunk order, adds the ZERO
-//                   donor's closed-form term and writes out/lse.  It is a
-//                   separate launch: the kernel boundary makes the partials
-//                   visible across XCDs without device-scope fences, whose
-//                   L2 write-back and invalidate cost every other work item
-//                   its cached prompt tiles.
+//   attn_kernel     splice_decode_attn, one launch per call, two kinds of
+//                   work item in one grid:
+//     prompt items  (KV head, 64 rows, prompt chunk): the rows are the
+//                   (cell, q head) pairs of all cells, clean cells first.
+//                   Each 64-key tile of the clean (and, for spliced rows,
+//                   the donor) prompt cache is staged in LDS once -- K
+//                   row-major, V transposed -- and feeds all 64 rows through
+//                   v_mfma_f32_16x16x32_bf16 for q.k and p.v.  (f32 inputs
+//                   take a per-cell vector-ALU variant.)
+//     generated items (cell, KV head, chunk of generated rows): lanes stream
+//                   the cell's own rows with coalesced 16-byte loads, D/16
+//                   lanes per row, v_dot2_f32_bf16 and a DPP butterfly for
+//                   q.k, per-row-group online softmax with lazy rescaling.
+//                   Generated rows are never spliced and are read once.
+//     Each item stores one partial (m, l, o) per row it serves; the last item
+//     of a (cell, KV head) to finish -- found with a device-scope counter --
+//     merges the partials and writes out and lse.
 //   fill_kernel     splice_workspace_init.
 //
 // ZERO donor: a ZERO slot has K = V = 0, so its score is exactly 0 and it
@@ -40,6 +40,8 @@
 #include <stdint.h>
 #include <string.h>
 
+#include <type_traits>
+
 #include "plan.hpp"
 #include "splice_attn.h"
 
@@ -47,10 +49,16 @@ namespace {
 
 constexpr int kThreads = 256;
 constexpr int kWaves = kThreads / 64;
+using splice::kMaxSlots;
+using splice::kRowBlock;
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
 
 typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
 
 __device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
@@ -136,91 +144,113 @@ __global__ __launch_bounds__(kThreads) void gather_kernel(GatherArgs a) {
 // --------------------------------------------------------------- attention
 
 struct AttnArgs {
-    const void *q;
+    const char *q;
     const char *ck, *cv, *dk, *dv, *gk, *gv;
-    float *out, *lse;
-    float *part;
-    int Hq, Hkv, Tp, cap, step;
-    int jp0, i0, sa, sb, n_gen;
+    float *out, *lse, *part;
+    int *counters;
+    uint32_t part_bytes;   // size of the partial-result region (< 2^31)
+    int C, Hq, Hkv, Tp, cap;
+    int jp0, i0, n_gen, sa, sb;
     int zero_donor;
-    int split, max_chunks, slot_floats;
+    int n_p, p_len, n_g, g_len, n_slots, slot_floats;
+    int n_rb, n_prompt_items, n_clean;
     float qk_scale;   // scale * log2(e)
     uint32_t spliced[SPLICE_MAX_CELLS / 32];
+    uint8_t order[SPLICE_MAX_CELLS];   // clean cells, then spliced cells
 };
 
-// Length of cell c's key list: visible prompt slots (without the ZERO slots of
-// a spliced cell, which never enter the list) plus visible generated rows.
-__device__ __forceinline__ int list_len(const AttnArgs &a, int c) {
-    const bool zskip = a.zero_donor && bit_set(a.spliced, c);
-    return (a.Tp - a.jp0) - (zskip ? a.sb - a.sa : 0) + a.n_gen;
+// Lazy rescaling: a running maximum is only raised when a score exceeds it
+// by more than this many powers of two, so weights stay <= 2^kSlack and the
+// rescale of the accumulators is rare.  The result is exact either way: a
+// partial result only needs its (m, l, o) to share one reference m.
+constexpr float kSlack = 8.f;
+
+// Partial results are written and read with the sc1 cache policy -- the
+// policy of agent-scope atomics: a store is written through to the device
+// coherence point before it counts as performed, and a load is served from
+// there rather than from a possibly stale L2 line of another XCD.  They go
+// through one buffer descriptor over the partial region (16-byte accesses;
+// dword 3 = 0x00020000 is the gfx9-family raw-buffer format).
+constexpr int kSc1 = 16;
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t part_rsrc(const AttnArgs &a) {
+    return __builtin_amdgcn_make_buffer_rsrc(a.part, 0, a.part_bytes, 0x00020000);
+}
+__device__ __forceinline__ void part_store4(__amdgpu_buffer_rsrc_t r, uint32_t off, f32x4_t v) {
+    __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4_t, v), r, off, 0, kSc1);
+}
+__device__ __forceinline__ void part_store1(__amdgpu_buffer_rsrc_t r, uint32_t off, float v) {
+    __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(v), r, off, 0, kSc1);
+}
+__device__ __forceinline__ f32x4_t part_load4(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+    return __builtin_bit_cast(f32x4_t, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, kSc1));
+}
+__device__ __forceinline__ float part_load1(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+    return __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(r, off, 0, kSc1));
 }
 
-// Lane layout for one K/V row of D elements (EB bytes each):
-//   LPK = D / 16 lanes per row ("row group"), KPW = 64 / LPK rows per wave;
-//   lane lj of a row group owns NP = EB pieces of 16 bytes at byte offsets
-//   p * (D * EB / NP) + lj * 16, i.e. 16 elements.  Each load instruction
-//   of a wave reads KPW rows x D bytes, fully coalesced.
+// LDS budget of one work group.
 template <int D, int G, bool BF16>
-__global__ __launch_bounds__(kThreads) void attn_kernel(AttnArgs a) {
-    constexpr int EB = BF16 ? 2 : 4;
-    constexpr int LPK = D / 16;
-    constexpr int KPW = 64 / LPK;
-    constexpr int NP = EB;
-    constexpr int EPP = 16 / EB;            // elements per piece
-    constexpr int PIECE_STRIDE = D * EB / NP;
-    constexpr int ROW_BYTES = D * EB;
-    constexpr int U = (BF16 && G <= 4) ? 4 : 2;   // rows per row group per iteration
-    constexpr int QW = BF16 ? 8 : 16;             // q registers per head per lane
+struct Lds {
+    static constexpr int KT = 64;                  // keys per staged prompt tile
+    static constexpr int KROW = D * 2 + 16;        // K tile row stride (bytes), padded
+    static constexpr int VROW = KT * 2 + 8;        // V^T tile row stride (bytes), padded
+    static constexpr int TILES = BF16 ? KT * KROW + D * VROW : 0;
+    static constexpr int MERGE = kWaves * G * (D + 2) * 4;
+    static constexpr int STAGE = 2 * kMaxSlots * kRowBlock * 4;
+    static constexpr int BYTES = TILES > MERGE ? (TILES > STAGE ? TILES : STAGE)
+                                               : (MERGE > STAGE ? MERGE : STAGE);
+};
 
-    __shared__ float s_o[kWaves][G][D];
-    __shared__ float s_m[kWaves][G];
-    __shared__ float s_l[kWaves][G];
+// ---------------------------------------------------------- vector-ALU rows
+//
+// Streams K/V rows [kbeg, kend) for the G query heads of one KV head.
+// Lane layout for a row of D elements of EB bytes: LPK = D / 16 lanes per
+// row (a "row group"), KPW = 64 / LPK row groups per wave; lane lj owns
+// NP = EB pieces of 16 bytes at byte offsets p * (D * EB / NP) + lj * 16, so
+// each load instruction of a wave covers KPW rows x D bytes without gaps.
+// A row group takes U consecutive rows per iteration and keeps its own
+// online-softmax state; row groups and waves are merged at the end.
+template <int D, int G, bool BF16>
+struct Valu {
+    static constexpr int EB = BF16 ? 2 : 4;
+    static constexpr int LPK = D / 16;
+    static constexpr int KPW = 64 / LPK;
+    static constexpr int NP = EB;
+    static constexpr int EPP = 16 / EB;
+    static constexpr int PIECE = D * EB / NP;
+    static constexpr int ROW = D * EB;
+    static constexpr int U = (BF16 && G <= 4) ? 4 : 2;
+    static constexpr int QW = BF16 ? 8 : 16;
+};
 
-    const int tid = threadIdx.x;
-    const int lane = tid & 63, wave = tid >> 6;
-    const int lj = lane % LPK, rg = lane / LPK;
-
-    int item = blockIdx.x;
-    const int ch = item % a.max_chunks;
-    item /= a.max_chunks;
-    const int g = item % a.Hkv;
-    const int c = item / a.Hkv;
-
-    const bool spl = bit_set(a.spliced, c);
-    const bool zskip = spl && a.zero_donor;
-    const int nsv = a.sb - a.sa;
-    const int n_prompt = (a.Tp - a.jp0) - (zskip ? nsv : 0);
-    const int n_list = n_prompt + a.n_gen;
-    const int n_chunks = (n_list + a.split - 1) / a.split;
-    if (ch >= n_chunks) return;
-    const int kbeg = ch * a.split;
-    const int kend = min(kbeg + a.split, n_list);
-
-    // q of the G heads of KV head g, this lane's 16 elements each
-    uint32_t qr[G][QW];
-    {
-        const char *qb = reinterpret_cast<const char *>(a.q) +
-                         ((size_t)c * a.Hq + (size_t)g * G) * ROW_BYTES;
+template <int D, int G, bool BF16>
+__device__ __forceinline__ void load_q(const AttnArgs &a, int c, int g, uint32_t (&qr)[G][Valu<D, G, BF16>::QW]) {
+    using V = Valu<D, G, BF16>;
+    const int lj = (threadIdx.x & 63) % V::LPK;
+    const char *qb = a.q + ((size_t)c * a.Hq + (size_t)g * G) * V::ROW;
 #pragma unroll
-        for (int h = 0; h < G; ++h)
+    for (int h = 0; h < G; ++h)
 #pragma unroll
-            for (int p = 0; p < NP; ++p) {
-                const uint4 w = *reinterpret_cast<const uint4 *>(qb + (size_t)h * ROW_BYTES +
-                                                                 p * PIECE_STRIDE + lj * 16);
-                qr[h][p * 4 + 0] = w.x; qr[h][p * 4 + 1] = w.y;
-                qr[h][p * 4 + 2] = w.z; qr[h][p * 4 + 3] = w.w;
-            }
-    }
+        for (int p = 0; p < V::NP; ++p) {
+            const uint4 w = *reinterpret_cast<const uint4 *>(qb + (size_t)h * V::ROW + p * V::PIECE + lj * 16);
+            qr[h][p * 4 + 0] = w.x;
+            qr[h][p * 4 + 1] = w.y;
+            qr[h][p * 4 + 2] = w.z;
+            qr[h][p * 4 + 3] = w.w;
+        }
+}
 
-    const size_t prompt_off = (size_t)g * a.Tp * ROW_BYTES;
-    const char *ckb = a.ck + prompt_off, *cvb = a.cv + prompt_off;
-    const char *dkb = a.zero_donor ? ckb : a.dk + prompt_off;
-    const char *dvb = a.zero_donor ? cvb : a.dv + prompt_off;
-    const size_t gen_off = ((size_t)c * a.Hkv + g) * (size_t)a.cap * ROW_BYTES;
-    const char *gkb = a.gk + gen_off, *gvb = a.gv + gen_off;
-
-    // online softmax state of this row group (identical in its LPK lanes)
-    float m[G], l[G], o[G][16];
+// row_of(key, &k_row, &v_row) -> false if the key is not to be attended
+// (its pointers must still be readable).
+template <int D, int G, bool BF16, class RowFn>
+__device__ __forceinline__ void valu_stream(const uint32_t (&qr)[G][Valu<D, G, BF16>::QW], int kbeg, int kend,
+                                            float qk_scale, RowFn row_of,
+                                            float (&m)[G], float (&l)[G], float (&o)[G][16]) {
+    using V = Valu<D, G, BF16>;
+    constexpr int U = V::U;
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int lj = lane % V::LPK, rg = lane / V::LPK;
 #pragma unroll
     for (int h = 0; h < G; ++h) {
         m[h] = -INFINITY;
@@ -228,35 +258,24 @@ __global__ __launch_bounds__(kThreads) void attn_kernel(AttnArgs a) {
 #pragma unroll
         for (int e = 0; e < 16; ++e) o[h][e] = 0.f;
     }
-
-    for (int base = kbeg + wave * (U * KPW); base < kend; base += kWaves * U * KPW) {
-        uint4 kr[U][NP], vr[U][NP];
-        bool valid[U];
+    for (int base = kbeg + wave * (V::KPW * U); base < kend; base += kWaves * V::KPW * U) {
+        const int kf = base + rg * U;
+        uint4 kr[U][V::NP], vr[U][V::NP];
+        bool ok[U];
 #pragma unroll
         for (int u = 0; u < U; ++u) {
-            int v = base + u * KPW + rg;
-            valid[u] = v < kend;
-            if (!valid[u]) v = kbeg;   // a row that exists; its score is masked below
-            const char *kp, *vp;
-            if (v < n_prompt) {
-                int j = v + a.jp0;
-                if (zskip && j >= a.sa) j += nsv;
-                const bool from_donor = spl && j >= a.sa && j < a.sb;
-                const size_t off = (size_t)j * ROW_BYTES;
-                kp = (from_donor ? dkb : ckb) + off;
-                vp = (from_donor ? dvb : cvb) + off;
-            } else {
-                const size_t off = (size_t)(a.i0 + (v - n_prompt)) * ROW_BYTES;
-                kp = gkb + off;
-                vp = gvb + off;
-            }
+            const int key = kf + u;
+            const bool inr = key < kend;
+            const char *kp;
+            const char *vp;
+            const bool use = row_of(inr ? key : kend - 1, kp, vp);
+            ok[u] = inr && use;
 #pragma unroll
-            for (int p = 0; p < NP; ++p) {
-                kr[u][p] = *reinterpret_cast<const uint4 *>(kp + p * PIECE_STRIDE + lj * 16);
-                vr[u][p] = *reinterpret_cast<const uint4 *>(vp + p * PIECE_STRIDE + lj * 16);
+            for (int p = 0; p < V::NP; ++p) {
+                kr[u][p] = *reinterpret_cast<const uint4 *>(kp + p * V::PIECE + lj * 16);
+                vr[u][p] = *reinterpret_cast<const uint4 *>(vp + p * V::PIECE + lj * 16);
             }
         }
-
         float s[U][G];
 #pragma unroll
         for (int u = 0; u < U; ++u)
@@ -264,50 +283,59 @@ __global__ __launch_bounds__(kThreads) void attn_kernel(AttnArgs a) {
             for (int h = 0; h < G; ++h) {
                 float acc = 0.f;
 #pragma unroll
-                for (int p = 0; p < NP; ++p) {
+                for (int p = 0; p < V::NP; ++p) {
                     const uint32_t kw[4] = {kr[u][p].x, kr[u][p].y, kr[u][p].z, kr[u][p].w};
 #pragma unroll
                     for (int i = 0; i < 4; ++i) {
-                        if constexpr (BF16) {
+                        if constexpr (BF16)
                             acc = dot2_bf16(qr[h][p * 4 + i], kw[i], acc);
-                        } else {
+                        else
                             acc = fmaf(__uint_as_float(qr[h][p * 4 + i]), __uint_as_float(kw[i]), acc);
-                        }
                     }
                 }
-                acc = group_sum<LPK>(acc) * a.qk_scale;
-                s[u][h] = valid[u] ? acc : -INFINITY;
+                acc = group_sum<V::LPK>(acc) * qk_scale;
+                s[u][h] = ok[u] ? acc : -INFINITY;
             }
-
-        // values of this lane's 16 elements for the U rows
         float vf[U][16];
 #pragma unroll
         for (int u = 0; u < U; ++u)
 #pragma unroll
-            for (int p = 0; p < NP; ++p) {
+            for (int p = 0; p < V::NP; ++p) {
                 const uint32_t vw[4] = {vr[u][p].x, vr[u][p].y, vr[u][p].z, vr[u][p].w};
 #pragma unroll
                 for (int i = 0; i < 4; ++i) {
                     if constexpr (BF16) {
-                        vf[u][p * EPP + 2 * i] = bf16_lo(vw[i]);
-                        vf[u][p * EPP + 2 * i + 1] = bf16_hi(vw[i]);
+                        vf[u][p * V::EPP + 2 * i] = bf16_lo(vw[i]);
+                        vf[u][p * V::EPP + 2 * i + 1] = bf16_hi(vw[i]);
                     } else {
-                        vf[u][p * EPP + i] = __uint_as_float(vw[i]);
+                        vf[u][p * V::EPP + i] = __uint_as_float(vw[i]);
                     }
                 }
             }
-
+        float mt[G];
+        bool need = false;
 #pragma unroll
         for (int h = 0; h < G; ++h) {
-            float mx = m[h];
+            mt[h] = s[0][h];
 #pragma unroll
-            for (int u = 0; u < U; ++u) mx = fmaxf(mx, s[u][h]);
-            const float ms = mx == -INFINITY ? 0.f : mx;
-            const float alpha = fast_exp2(m[h] - ms);
-            l[h] *= alpha;
+            for (int u = 1; u < U; ++u) mt[h] = fmaxf(mt[h], s[u][h]);
+            need |= mt[h] > m[h] + kSlack;
+        }
+        if (__any(need)) {
 #pragma unroll
-            for (int e = 0; e < 16; ++e) o[h][e] *= alpha;
-            m[h] = mx;
+            for (int h = 0; h < G; ++h) {
+                const bool nh = mt[h] > m[h] + kSlack;
+                const float mn = nh ? fmaxf(m[h], mt[h]) : m[h];
+                const float al = nh ? fast_exp2(m[h] - (mn == -INFINITY ? 0.f : mn)) : 1.f;
+                l[h] *= al;
+#pragma unroll
+                for (int e = 0; e < 16; ++e) o[h][e] *= al;
+                m[h] = mn;
+            }
+        }
+#pragma unroll
+        for (int h = 0; h < G; ++h) {
+            const float ms = m[h] == -INFINITY ? 0.f : m[h];
 #pragma unroll
             for (int u = 0; u < U; ++u) {
                 const float pw = fast_exp2(s[u][h] - ms);
@@ -317,10 +345,22 @@ __global__ __launch_bounds__(kThreads) void attn_kernel(AttnArgs a) {
             }
         }
     }
+}
 
-    // merge the KPW row-group states of this wave (butterfly over lanes)
+// Merge the row groups of each wave (lane butterfly) and the waves (LDS),
+// then store the work item's partial result into `slot` with agent-scope
+// stores: o[G][D], m[G], l[G].
+template <int D, int G, bool BF16>
+__device__ __forceinline__ void valu_store_partial(const AttnArgs &a, float (&m)[G], float (&l)[G], float (&o)[G][16],
+                                                   char *buf, uint32_t slot) {
+    using V = Valu<D, G, BF16>;
+    float *s_o = reinterpret_cast<float *>(buf);              // [kWaves][G][D]
+    float *s_m = s_o + kWaves * G * D;                         // [kWaves][G]
+    float *s_l = s_m + kWaves * G;                             // [kWaves][G]
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int lj = lane % V::LPK, rg = lane / V::LPK;
 #pragma unroll
-    for (int off = LPK; off < 64; off <<= 1) {
+    for (int off = V::LPK; off < 64; off <<= 1) {
 #pragma unroll
         for (int h = 0; h < G; ++h) {
             const float mo = __shfl_xor(m[h], off);
@@ -330,94 +370,518 @@ __global__ __launch_bounds__(kThreads) void attn_kernel(AttnArgs a) {
             const float fa = fast_exp2(m[h] - ms), fb = fast_exp2(mo - ms);
             l[h] = l[h] * fa + lo * fb;
 #pragma unroll
-            for (int e = 0; e < 16; ++e) {
-                const float oo = __shfl_xor(o[h][e], off);
-                o[h][e] = o[h][e] * fa + oo * fb;
-            }
+            for (int e = 0; e < 16; ++e) o[h][e] = o[h][e] * fa + __shfl_xor(o[h][e], off) * fb;
             m[h] = mx;
         }
     }
+    __syncthreads();   // buf may still be read by a previous phase
     if (rg == 0) {
 #pragma unroll
         for (int h = 0; h < G; ++h) {
 #pragma unroll
-            for (int p = 0; p < NP; ++p)
+            for (int p = 0; p < V::NP; ++p)
 #pragma unroll
-                for (int i = 0; i < EPP; ++i)
-                    s_o[wave][h][p * (D / NP) + lj * EPP + i] = o[h][p * EPP + i];
+                for (int i = 0; i < V::EPP; ++i)
+                    s_o[(wave * G + h) * D + p * (D / V::NP) + lj * V::EPP + i] = o[h][p * V::EPP + i];
             if (lj == 0) {
-                s_m[wave][h] = m[h];
-                s_l[wave][h] = l[h];
+                s_m[wave * G + h] = m[h];
+                s_l[wave * G + h] = l[h];
             }
         }
     }
     __syncthreads();
-
-    // merge the waves; a single-chunk list finishes here, otherwise the
-    // work item writes its partial slot
-    const bool zero_term = zskip && nsv > 0;
-    const int row0 = c * a.Hq + g * G;
-    float *slot_base = a.part + ((size_t)(c * a.Hkv + g) * a.max_chunks) * a.slot_floats;
-    for (int e = tid; e < G * D; e += kThreads) {
-        const int h = e / D, d = e % D;
+    const __amdgpu_buffer_rsrc_t r = part_rsrc(a);
+    for (int e = tid; e < G * D / 4; e += kThreads) {   // four consecutive d per thread
+        const int h = e / (D / 4), d = 4 * (e % (D / 4));
         float M = -INFINITY;
 #pragma unroll
-        for (int w = 0; w < kWaves; ++w) M = fmaxf(M, s_m[w][h]);
+        for (int w = 0; w < kWaves; ++w) M = fmaxf(M, s_m[w * G + h]);
         const float Ms = M == -INFINITY ? 0.f : M;
-        float L = 0.f, O = 0.f;
+        float L = 0.f;
+        f32x4_t O = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int w = 0; w < kWaves; ++w) {
-            const float f = fast_exp2(s_m[w][h] - Ms);
-            L = fmaf(s_l[w][h], f, L);
-            O = fmaf(s_o[w][h][d], f, O);
+            const float f = fast_exp2(s_m[w * G + h] - Ms);
+            L = fmaf(s_l[w * G + h], f, L);
+            O += *reinterpret_cast<const f32x4_t *>(s_o + (w * G + h) * D + d) * f;
         }
-        if (n_chunks == 1) {
-            if (zero_term) {
-                const float Mz = fmaxf(M, 0.f);
-                const float f = fast_exp2(M - Mz);
-                L = L * f + (float)nsv * fast_exp2(-Mz);
-                O *= f;
-                M = Mz;
-            }
-            a.out[(size_t)(row0 + h) * D + d] = O / L;
-            if (d == 0) a.lse[row0 + h] = (M + log2f(L)) * kLn2;
-        } else {
-            float *slot = slot_base + (size_t)ch * a.slot_floats;
-            slot[h * D + d] = O;
-            if (d == 0) {
-                slot[G * D + h] = M;
-                slot[G * D + G + h] = L;
-            }
+        part_store4(r, slot + (uint32_t)(h * D + d) * 4u, O);
+        if (d == 0) {
+            part_store1(r, slot + (uint32_t)(G * D + h) * 4u, M);
+            part_store1(r, slot + (uint32_t)(G * D + G + h) * 4u, L);
         }
     }
 }
 
-// Merge the partials of one (cell, KV head) in chunk order (grid: C * Hkv).
-template <int D, int G>
-__global__ __launch_bounds__(kThreads) void combine_kernel(AttnArgs a) {
-    const int g = blockIdx.x % a.Hkv;
-    const int c = blockIdx.x / a.Hkv;
-    const int n_chunks = (list_len(a, c) + a.split - 1) / a.split;
-    if (n_chunks <= 1) return;   // finished by the attention kernel
-    const bool zero_term = a.zero_donor && bit_set(a.spliced, c) && a.sb > a.sa;
-    const float nsv = (float)(a.sb - a.sa);
-    const float *slot_base = a.part + ((size_t)(c * a.Hkv + g) * a.max_chunks) * a.slot_floats;
-    const int row0 = c * a.Hq + g * G;
-    for (int e = threadIdx.x; e < G * D; e += kThreads) {
-        const int h = e / D, d = e % D;
-        float M = zero_term ? 0.f : -INFINITY;
-        for (int k = 0; k < n_chunks; ++k)
-            M = fmaxf(M, slot_base[(size_t)k * a.slot_floats + G * D + h]);
-        float L = zero_term ? nsv * fast_exp2(-M) : 0.f;
-        float O = 0.f;
-        for (int k = 0; k < n_chunks; ++k) {
-            const float *slot = slot_base + (size_t)k * a.slot_floats;
-            const float f = fast_exp2(slot[G * D + h] - M);
-            L = fmaf(slot[G * D + G + h], f, L);
-            O = fmaf(slot[h * D + d], f, O);
+// Byte offset of slot k of (cell c, KV head g) in the partial region.
+__device__ __forceinline__ uint32_t slot_off(const AttnArgs &a, int c, int g, int k) {
+    return (uint32_t)((((c * a.Hkv + g) * a.n_slots) + k) * a.slot_floats) * 4u;
+}
+
+// Generated rows of one (cell, KV head): contiguous, never spliced.
+template <int D, int G, bool BF16>
+__device__ void gen_item(const AttnArgs &a, int c, int g, int gk, char *buf) {
+    using V = Valu<D, G, BF16>;
+    uint32_t qr[G][V::QW];
+    load_q<D, G, BF16>(a, c, g, qr);
+    const int r0 = a.i0 + gk * a.g_len;
+    const int r1 = min(r0 + a.g_len, a.i0 + a.n_gen);
+    const size_t off = ((size_t)c * a.Hkv + g) * (size_t)a.cap * V::ROW;
+    const char *kb = a.gk + off, *vb = a.gv + off;
+    float m[G], l[G], o[G][16];
+    valu_stream<D, G, BF16>(qr, r0, r1, a.qk_scale,
+                            [&](int key, const char *&kp, const char *&vp) {
+                                kp = kb + (size_t)key * V::ROW;
+                                vp = vb + (size_t)key * V::ROW;
+                                return true;
+                            },
+                            m, l, o);
+    valu_store_partial<D, G, BF16>(a, m, l, o, buf, slot_off(a, c, g, a.n_p + gk));
+}
+
+// Prompt chunk of one (cell, KV head) on the vector ALUs (f32 inputs): each
+// key is read from the clean or the donor cache by pointer; ZERO slots are
+// skipped (their closed-form term is added when the partials are merged).
+template <int D, int G, bool BF16>
+__device__ void prompt_item_valu(const AttnArgs &a, int c, int g, int pk, char *buf) {
+    using V = Valu<D, G, BF16>;
+    uint32_t qr[G][V::QW];
+    load_q<D, G, BF16>(a, c, g, qr);
+    const int k0 = a.jp0 + pk * a.p_len;
+    const int k1 = min(k0 + a.p_len, a.Tp);
+    const bool spl = bit_set(a.spliced, c);
+    const size_t head = (size_t)g * a.Tp * V::ROW;
+    float m[G], l[G], o[G][16];
+    valu_stream<D, G, BF16>(qr, k0, k1, a.qk_scale,
+                            [&](int j, const char *&kp, const char *&vp) {
+                                const bool in_span = j >= a.sa && j < a.sb;
+                                const bool donor = spl && in_span && !a.zero_donor;
+                                const size_t off = head + (size_t)j * V::ROW;
+                                kp = (donor ? a.dk : a.ck) + off;
+                                vp = (donor ? a.dv : a.cv) + off;
+                                return !(spl && in_span && a.zero_donor);
+                            },
+                            m, l, o);
+    valu_store_partial<D, G, BF16>(a, m, l, o, buf, slot_off(a, c, g, pk));
+}
+
+// ------------------------------------------------------- MFMA prompt rows
+//
+// One prompt chunk [k0, k1) for kRowBlock = 64 rows of one KV head; wave w
+// owns rows 16w..16w+15, lane (col = l % 16, quad = l / 16) owns row col.
+// Per tile of 64 keys (and per source: clean pass, then donor pass when the
+// block has spliced rows and the tile touches the span):
+//   * K rows and the transposed V tile are staged in LDS once, for all rows;
+//   * S^T (keys x rows) = K Q^T with v_mfma_f32_16x16x32_bf16 (A = K from
+//     LDS, B = this lane's q fragment); lane holds keys 16 sub + 4 quad + i;
+//   * masks: key in the chunk, and the key belongs to this pass for this
+//     row (non-span keys and the span of clean rows read clean; the span of
+//     spliced rows reads the donor; ZERO rows skip the span);
+//   * online softmax with a shared row maximum (4 quads), lazy rescale;
+//   * O^T (d x rows) += V^T P^T, P split into bf16 hi + lo parts so the
+//     weights keep ~16 significant bits.  Lane holds O^T[16 dt + 4 quad + i]
+//     for its own row, so the rescale by the row's factor is lane-local.
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+
+// One thread's share of staging a KT-key prompt tile: K in 16-byte units
+// (row-major in LDS), V in units of 4 keys x 8 d (transposed in LDS, so the
+// p.v operand reads key-contiguous words).
+template <int D>
+struct TileIo {
+    static constexpr int KT = 64;
+    static constexpr int KROW = D * 2 + 16;
+    static constexpr int VROW = KT * 2 + 8;
+    static constexpr int KUNITS = KT * (D / 8);
+    static constexpr int VUNITS = (D / 8) * (KT / 4);
+    static constexpr int NKU = KUNITS / kThreads;
+    static constexpr int NVU = VUNITS >= kThreads ? VUNITS / kThreads : 1;
+};
+
+// Compile-time loop: f(std::integral_constant<int, I>) for I in [B, E), so
+// register arrays are only ever indexed by constants.
+template <int B, int E, class F>
+__device__ __forceinline__ void static_for(F &&f) {
+    if constexpr (B < E) {
+        f(std::integral_constant<int, B>{});
+        static_for<B + 1, E>(f);
+    }
+}
+
+template <int D>
+__device__ __forceinline__ void tile_fetch(u32x4_t (&kreg)[TileIo<D>::NKU], u32x4_t (&vreg)[TileIo<D>::NVU][4],
+                                           const char *Kg, const char *Vg, int t0, int t1) {
+    using T = TileIo<D>;
+    const int tid = threadIdx.x;
+    static_for<0, T::NKU>([&](auto n) {
+        const int u = tid + n * kThreads;
+        const int r = u / (D / 8), part = u % (D / 8);
+        const int key = min(t0 + r, t1 - 1);
+        kreg[n] = *reinterpret_cast<const u32x4_t *>(Kg + (size_t)key * (D * 2) + part * 16);
+    });
+    static_for<0, T::NVU>([&](auto n) {
+        const int u = tid + n * kThreads;
+        const int dg = u % (D / 8), kq = (u / (D / 8)) % (T::KT / 4);   // in range for every lane
+        static_for<0, 4>([&](auto kk) {
+            const int key = min(t0 + 4 * kq + kk, t1 - 1);
+            vreg[n][kk] = *reinterpret_cast<const u32x4_t *>(Vg + (size_t)key * (D * 2) + dg * 16);
+        });
+    });
+}
+
+template <int D>
+__device__ __forceinline__ void tile_stage(const u32x4_t (&kreg)[TileIo<D>::NKU], const u32x4_t (&vreg)[TileIo<D>::NVU][4],
+                                           char *sK, char *sV) {
+    using T = TileIo<D>;
+    const int tid = threadIdx.x;
+    static_for<0, T::NKU>([&](auto n) {
+        const int u = tid + n * kThreads;
+        const int r = u / (D / 8), part = u % (D / 8);
+        *reinterpret_cast<u32x4_t *>(sK + r * T::KROW + part * 16) = kreg[n];
+    });
+    static_for<0, T::NVU>([&](auto n) {
+        const int u = tid + n * kThreads;
+        if (u < T::VUNITS) {
+            const int dg = u % (D / 8), kq = u / (D / 8);
+            static_for<0, 8>([&](auto j) {
+                constexpr int jj = decltype(j)::value;
+                constexpr uint32_t sel = (jj & 1) ? 0x07060302u : 0x05040100u;
+                const uint32_t lo = __builtin_amdgcn_perm(vreg[n][1][jj >> 1], vreg[n][0][jj >> 1], sel);
+                const uint32_t hi = __builtin_amdgcn_perm(vreg[n][3][jj >> 1], vreg[n][2][jj >> 1], sel);
+                *reinterpret_cast<u32x2_t *>(sV + (8 * dg + jj) * T::VROW + 8 * kq) = u32x2_t{lo, hi};
+            });
         }
-        a.out[(size_t)(row0 + h) * D + d] = O / L;
-        if (d == 0) a.lse[row0 + h] = (M + log2f(L)) * kLn2;
+    });
+}
+
+template <int D, int G>
+__device__ void prompt_item_mfma(const AttnArgs &a, int g, int rb, int pk, char *buf) {
+    using L = Lds<D, G, true>;
+    constexpr int KT = L::KT, KROW = L::KROW, VROW = L::VROW;
+    constexpr int NDS = D / 32;   // k-steps of q.k
+    constexpr int NDT = D / 16;   // 16-wide d tiles of the output
+    char *sK = buf;
+    char *sV = buf + KT * KROW;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int col = lane & 15, quad = lane >> 4;
+
+    const int R = rb * kRowBlock + wave * 16 + col;
+    const int cidx = R / G;
+    const bool row_ok = cidx < a.C;
+    const int cell = row_ok ? a.order[cidx] : 0;
+    const int hl = R % G;
+    const bool spl = row_ok && bit_set(a.spliced, cell);
+    const bool row_clean = row_ok && !spl;
+    const bool row_donor = spl && !a.zero_donor;
+    const int first = rb * kRowBlock / G;
+    const int last = min(a.C, (rb + 1) * kRowBlock / G) - 1;
+    const bool blk_clean = first < a.n_clean;
+    const bool blk_donor = !a.zero_donor && last >= a.n_clean;
+
+    bf16x8_t qf[NDS];
+    {
+        const char *qrow = a.q + ((size_t)cell * a.Hq + (size_t)g * G + hl) * (D * 2);
+        static_for<0, NDS>([&](auto st) {
+            uint4 w = make_uint4(0, 0, 0, 0);
+            if (row_ok) w = *reinterpret_cast<const uint4 *>(qrow + (32 * st + 8 * quad) * 2);
+            qf[st] = __builtin_bit_cast(bf16x8_t, w);
+        });
+    }
+    f32x4_t o[NDT];
+    static_for<0, NDT>([&](auto t) { o[t] = f32x4_t{0.f, 0.f, 0.f, 0.f}; });
+    float m = -INFINITY, lsum = 0.f;
+
+    const int k0 = a.jp0 + pk * a.p_len;
+    const int k1 = min(k0 + a.p_len, a.Tp);
+    const size_t head = (size_t)g * a.Tp * (D * 2);
+
+    // The chunk is a sequence of steps (tile, source).  Tiles hold up to KT
+    // keys and never straddle a span boundary (a tile is all span or all
+    // not), so a row's keys are grouped the same whether it is spliced or
+    // not.  A tile runs a clean pass if any row reads it from the clean cache
+    // and a donor pass if any spliced row reads it from the donor cache.
+    auto tile_end = [&](int t0) __attribute__((always_inline)) {
+        int t1 = min(t0 + KT, k1);
+        if (t0 < a.sa) t1 = min(t1, a.sa);
+        else if (t0 < a.sb) t1 = min(t1, a.sb);
+        return t1;
+    };
+    auto needed = [&](int t0, int dpass) __attribute__((always_inline)) {
+        const bool span = t0 >= a.sa && t0 < a.sb;
+        return dpass ? (span && blk_donor) : (!span || blk_clean);
+    };
+    auto advance = [&](int &t0, int &dpass) __attribute__((always_inline)) {   // to the next needed step, t0 = k1 at the end
+        for (;;) {
+            if (dpass == 0) {
+                dpass = 1;
+            } else {
+                t0 = tile_end(t0);
+                dpass = 0;
+            }
+            if (t0 >= k1 || needed(t0, dpass)) return;
+        }
+    };
+
+    // this thread's share of a tile: K units (16 bytes) and V units (4 keys x 8 d)
+    u32x4_t kreg[TileIo<D>::NKU];
+    u32x4_t vreg[TileIo<D>::NVU][4];
+
+    int t0 = k0, dpass = 0;
+    if (t0 < k1 && !needed(t0, 0)) advance(t0, dpass);
+    if (t0 < k1)
+        tile_fetch<D>(kreg, vreg, (dpass ? a.dk : a.ck) + head, (dpass ? a.dv : a.cv) + head, t0, tile_end(t0));
+    while (t0 < k1) {
+        const int t1 = tile_end(t0);
+        const int cur_dpass = dpass;
+        __syncthreads();   // the previous step no longer reads the LDS tiles
+        tile_stage<D>(kreg, vreg, sK, sV);
+        __syncthreads();
+        int nt0 = t0, ndpass = dpass;
+        advance(nt0, ndpass);
+        if (nt0 < k1)   // in flight while this step computes
+            tile_fetch<D>(kreg, vreg, (ndpass ? a.dk : a.ck) + head, (ndpass ? a.dv : a.cv) + head, nt0,
+                          tile_end(nt0));
+
+        f32x4_t s[4];
+        static_for<0, 4>([&](auto sub) {
+            s[sub] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+            static_for<0, NDS>([&](auto st) {
+                const bf16x8_t kf = *reinterpret_cast<const bf16x8_t *>(
+                    sK + (16 * sub + col) * KROW + (32 * st + 8 * quad) * 2);
+                s[sub] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[st], s[sub], 0, 0, 0);
+            });
+        });
+        float p[4][4];
+        float mt = -INFINITY;
+#pragma unroll
+        for (int sub = 0; sub < 4; ++sub)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int key = t0 + 16 * sub + 4 * quad + i;
+                const bool in_span = key >= a.sa && key < a.sb;
+                const bool ok = row_ok && key < t1 &&
+                                (cur_dpass ? (in_span && row_donor) : (!in_span || row_clean));
+                p[sub][i] = ok ? s[sub][i] * a.qk_scale : -INFINITY;
+                mt = fmaxf(mt, p[sub][i]);
+            }
+        mt = fmaxf(mt, __shfl_xor(mt, 16));
+        mt = fmaxf(mt, __shfl_xor(mt, 32));
+        const bool need = mt > m + kSlack;
+        if (__any(need)) {
+            // only rows that need it move their maximum: a row's arithmetic
+            // never depends on the other rows of its wave
+            const float mn = need ? fmaxf(m, mt) : m;
+            const float al = need ? fast_exp2(m - (mn == -INFINITY ? 0.f : mn)) : 1.f;
+            lsum *= al;
+            static_for<0, NDT>([&](auto t) { o[t] *= al; });
+            m = mn;
+        }
+        const float ms = m == -INFINITY ? 0.f : m;
+#pragma unroll
+        for (int sub = 0; sub < 4; ++sub)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                p[sub][i] = fast_exp2(p[sub][i] - ms);
+                lsum += p[sub][i];
+            }
+        static_for<0, 2>([&](auto kg) {
+            bf16x8_t ph, pl;
+            static_for<0, 8>([&](auto j) {
+                constexpr int jj = decltype(j)::value;
+                const float x = p[2 * kg + (jj >> 2)][jj & 3];
+                const __bf16 hb = (__bf16)x;
+                ph[jj] = hb;
+                pl[jj] = (__bf16)(x - (float)hb);
+            });
+            static_for<0, NDT>([&](auto t) {
+                const char *vrow = sV + (16 * t + col) * VROW;
+                const uint2 va = *reinterpret_cast<const uint2 *>(vrow + (32 * kg + 4 * quad) * 2);
+                const uint2 vb = *reinterpret_cast<const uint2 *>(vrow + (32 * kg + 16 + 4 * quad) * 2);
+                const bf16x8_t vf = __builtin_bit_cast(bf16x8_t, make_uint4(va.x, va.y, vb.x, vb.y));
+                o[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, ph, o[t], 0, 0, 0);
+                o[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pl, o[t], 0, 0, 0);
+            });
+        });
+        t0 = nt0;
+        dpass = ndpass;
+    }
+    lsum += __shfl_xor(lsum, 16);
+    lsum += __shfl_xor(lsum, 32);
+    if (row_ok) {
+        const __amdgpu_buffer_rsrc_t r = part_rsrc(a);
+        const uint32_t slot = slot_off(a, cell, g, pk);
+        static_for<0, NDT>([&](auto t) {
+            part_store4(r, slot + (uint32_t)(hl * D + 16 * t + 4 * quad) * 4u, o[t]);
+        });
+        if (quad == 0) {
+            part_store1(r, slot + (uint32_t)(G * D + hl) * 4u, m);
+            part_store1(r, slot + (uint32_t)(G * D + G + hl) * 4u, lsum);
+        }
+    }
+}
+
+// ----------------------------------------------------------- merging
+//
+// Every work item stores its partial results with agent-scope (L2
+// write-through) stores, waits until they are performed, and then counts
+// itself on each (cell, KV head) it fed with a device-scope atomic.  The item
+// that brings a counter to n_slots merges that (cell, KV head): it reads the
+// slots with agent-scope loads (which do not trust a stale L2 line), merges
+// them in slot order with a log-sum-exp combine, adds the ZERO term, writes
+// out and lse, and re-arms the counter.  No cache-wide write-back or
+// invalidate is needed, so the cached tiles of other items survive.
+
+__device__ __forceinline__ void stores_performed() {
+    __builtin_amdgcn_s_waitcnt(0);   // every outstanding memory operation of this lane is done
+    __syncthreads();
+}
+
+__device__ __forceinline__ bool arrive(const AttnArgs &a, int c, int g) {
+    const int prev = __hip_atomic_fetch_add(&a.counters[c * a.Hkv + g], 1, __ATOMIC_RELAXED,
+                                            __HIP_MEMORY_SCOPE_AGENT);
+    return prev == a.n_slots - 1;
+}
+
+// Merge the partial results of cells list[0..n) of KV head g.  One round of
+// loads stages every (m, l) in LDS; then each thread owns up to kMergeUnits
+// groups of four consecutive outputs and loads them two slots at a time, so
+// a merge costs a few memory round trips whatever the cell count.
+constexpr int kMergeUnits = 4;
+
+template <int D, int G>
+__device__ void combine_cells(const AttnArgs &a, const int *list, int n, int g, char *buf) {
+    const __amdgpu_buffer_rsrc_t r = part_rsrc(a);
+    float *s_m = reinterpret_cast<float *>(buf);           // [n][n_slots][G]
+    float *s_l = s_m + kRowBlock * kMaxSlots;               // [n][n_slots][G]
+    const int per_cell = a.n_slots * G;
+    for (int t = threadIdx.x; t < n * per_cell; t += kThreads) {
+        const int i = t / per_cell, rem = t % per_cell;
+        const int k = rem / G, h = rem % G;
+        const uint32_t slot = slot_off(a, list[i], g, k);
+        s_m[t] = part_load1(r, slot + (uint32_t)(G * D + h) * 4u);
+        s_l[t] = part_load1(r, slot + (uint32_t)(G * D + G + h) * 4u);
+    }
+    __syncthreads();
+    constexpr int UPC = G * D / 4;                           // 4-wide units per cell
+    const int total = n * UPC;
+    const uint32_t slot_bytes = (uint32_t)a.slot_floats * 4u;
+    for (int u0 = threadIdx.x; u0 < total; u0 += kThreads * kMergeUnits) {
+        float M[kMergeUnits], L[kMergeUnits];
+        f32x4_t O[kMergeUnits];
+        uint32_t base[kMergeUnits];
+        int sm_off[kMergeUnits];
+#pragma unroll
+        for (int b = 0; b < kMergeUnits; ++b) {
+            const int u = min(u0 + b * kThreads, total - 1);   // tail units repeat a valid one
+            const int i = u / UPC, rem = u % UPC;
+            const int h = rem / (D / 4), d = 4 * (rem % (D / 4));
+            const int c = list[i];
+            sm_off[b] = i * per_cell + h;
+            base[b] = slot_off(a, c, g, 0) + (uint32_t)(h * D + d) * 4u;
+            const bool zero_term = a.zero_donor && bit_set(a.spliced, c) && a.sb > a.sa;
+            float mx = zero_term ? 0.f : -INFINITY;
+            for (int k = 0; k < a.n_slots; ++k) mx = fmaxf(mx, s_m[sm_off[b] + k * G]);
+            M[b] = mx;
+            L[b] = zero_term ? (float)(a.sb - a.sa) * fast_exp2(-mx) : 0.f;
+            O[b] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+        }
+        int k = 0;
+        for (; k + 2 <= a.n_slots; k += 2) {
+            f32x4_t v0[kMergeUnits], v1[kMergeUnits];
+#pragma unroll
+            for (int b = 0; b < kMergeUnits; ++b) {
+                v0[b] = part_load4(r, base[b] + (uint32_t)k * slot_bytes);
+                v1[b] = part_load4(r, base[b] + (uint32_t)(k + 1) * slot_bytes);
+            }
+#pragma unroll
+            for (int b = 0; b < kMergeUnits; ++b) {
+                const float f0 = fast_exp2(s_m[sm_off[b] + k * G] - M[b]);
+                const float f1 = fast_exp2(s_m[sm_off[b] + (k + 1) * G] - M[b]);
+                L[b] = fmaf(s_l[sm_off[b] + k * G], f0, L[b]);
+                L[b] = fmaf(s_l[sm_off[b] + (k + 1) * G], f1, L[b]);
+                O[b] += v0[b] * f0;
+                O[b] += v1[b] * f1;
+            }
+        }
+        if (k < a.n_slots) {
+            f32x4_t v0[kMergeUnits];
+#pragma unroll
+            for (int b = 0; b < kMergeUnits; ++b) v0[b] = part_load4(r, base[b] + (uint32_t)k * slot_bytes);
+#pragma unroll
+            for (int b = 0; b < kMergeUnits; ++b) {
+                const float f0 = fast_exp2(s_m[sm_off[b] + k * G] - M[b]);
+                L[b] = fmaf(s_l[sm_off[b] + k * G], f0, L[b]);
+                O[b] += v0[b] * f0;
+            }
+        }
+#pragma unroll
+        for (int b = 0; b < kMergeUnits; ++b) {
+            const int u = u0 + b * kThreads;
+            if (u < total) {
+                const int i = u / UPC, rem = u % UPC;
+                const int h = rem / (D / 4), d = 4 * (rem % (D / 4));
+                const int row = list[i] * a.Hq + g * G + h;
+                *reinterpret_cast<f32x4_t *>(a.out + (size_t)row * D + d) = O[b] * (1.f / L[b]);
+                if (d == 0) a.lse[row] = (M[b] + log2f(L[b])) * kLn2;
+            }
+        }
+    }
+    if (threadIdx.x < n)
+        __hip_atomic_store(&a.counters[list[threadIdx.x] * a.Hkv + g], 0, __ATOMIC_RELAXED,
+                           __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// One launch per call: blocks [0, n_prompt_items) are prompt items, the
+// rest generated-row items.
+template <int D, int G, bool BF16>
+__global__ __launch_bounds__(kThreads) void attn_kernel(AttnArgs a) {
+    __shared__ __attribute__((aligned(16))) char buf[Lds<D, G, BF16>::BYTES];
+    __shared__ int s_list[kRowBlock + 1];
+    const int tid = threadIdx.x;
+    int item = blockIdx.x;
+    if (item < a.n_prompt_items) {
+        const int pk = item % a.n_p;
+        item /= a.n_p;
+        if constexpr (BF16) {
+            const int rb = item % a.n_rb;
+            const int g = item / a.n_rb;
+            prompt_item_mfma<D, G>(a, g, rb, pk, buf);
+            if (tid == 0) s_list[0] = 0;
+            stores_performed();
+            const int first = rb * kRowBlock / G;
+            const int n_cells = min(a.C, first + kRowBlock / G) - first;
+            if (tid < n_cells) {
+                const int cell = a.order[first + tid];
+                if (arrive(a, cell, g)) s_list[1 + atomicAdd(&s_list[0], 1)] = cell;
+            }
+            __syncthreads();
+            if (s_list[0] > 0) combine_cells<D, G>(a, s_list + 1, s_list[0], g, buf);
+        } else {
+            const int g = item % a.Hkv;
+            const int c = item / a.Hkv;
+            prompt_item_valu<D, G, BF16>(a, c, g, pk, buf);
+            stores_performed();
+            if (tid == 0) {
+                s_list[0] = arrive(a, c, g) ? 1 : 0;
+                s_list[1] = c;
+            }
+            __syncthreads();
+            if (s_list[0]) combine_cells<D, G>(a, s_list + 1, 1, g, buf);
+        }
+    } else {
+        item -= a.n_prompt_items;
+        const int gk = item % a.n_g;
+        item /= a.n_g;
+        const int g = item % a.Hkv;
+        const int c = item / a.Hkv;
+        gen_item<D, G, BF16>(a, c, g, gk, buf);
+        stores_performed();
+        if (tid == 0) {
+            s_list[0] = arrive(a, c, g) ? 1 : 0;
+            s_list[1] = c;
+        }
+        __syncthreads();
+        if (s_list[0]) combine_cells<D, G>(a, s_list + 1, 1, g, buf);
     }
 }
 
@@ -430,37 +894,29 @@ __global__ __launch_bounds__(kThreads) void fill_kernel(uint32_t *p, size_t n_wo
 // ------------------------------------------------------------ dispatch
 
 typedef void (*attn_fn)(AttnArgs);
-struct AttnKernels {
-    attn_fn attn, combine;
-};
-
-template <int D, int G, bool BF16>
-AttnKernels kernels_of() {
-    return AttnKernels{attn_kernel<D, G, BF16>, combine_kernel<D, G>};
-}
 
 template <int D, bool BF16>
-AttnKernels pick_g(int G) {
+attn_fn pick_g(int G) {
     switch (G) {
-    case 1: return kernels_of<D, 1, BF16>();
-    case 2: return kernels_of<D, 2, BF16>();
-    case 4: return kernels_of<D, 4, BF16>();
-    case 8: return kernels_of<D, 8, BF16>();
-    default: return AttnKernels{nullptr, nullptr};
+    case 1: return attn_kernel<D, 1, BF16>;
+    case 2: return attn_kernel<D, 2, BF16>;
+    case 4: return attn_kernel<D, 4, BF16>;
+    case 8: return attn_kernel<D, 8, BF16>;
+    default: return nullptr;
     }
 }
 
 template <bool BF16>
-AttnKernels pick_d(int D, int G) {
+attn_fn pick_d(int D, int G) {
     switch (D) {
     case 64: return pick_g<64, BF16>(G);
     case 128: return pick_g<128, BF16>(G);
     case 256: return pick_g<256, BF16>(G);
-    default: return AttnKernels{nullptr, nullptr};
+    default: return nullptr;
     }
 }
 
-AttnKernels pick_attn(int D, int G, int dtype) {
+attn_fn pick_attn(int D, int G, int dtype) {
     return dtype == SPLICE_BF16 ? pick_d<true>(D, G) : pick_d<false>(D, G);
 }
 
@@ -468,12 +924,6 @@ void fill_mask(const splice_shape &sh, const splice_call &call, const int32_t *c
     for (int i = 0; i < SPLICE_MAX_CELLS / 32; ++i) mask[i] = 0u;
     for (int c = 0; c < sh.n_cells; ++c)
         if (splice::cell_spliced(cell_LW, c, call.layer, call.step)) mask[c >> 5] |= 1u << (c & 31);
-}
-
-int plan_chunks(const splice_shape &sh, const splice_call &call, const splice::Geometry &geo, int *split) {
-    *split = call.split_keys > 0 ? call.split_keys
-                                 : splice::default_split(geo.n_vis, sh.n_cells, sh.n_kv_heads);
-    return splice::ceil_div(geo.n_vis, *split);
 }
 
 int32_t launch_status() {
@@ -554,16 +1004,16 @@ int32_t splice_kv_build(const splice_shape *shape, const splice_call *call, cons
 int64_t splice_decode_attn_workspace_bytes(const splice_shape *shape, const splice_call *call) {
     int32_t rc = splice::validate_shape(shape);
     if (rc != SPLICE_OK) return rc;
-    int max_chunks;
+    int n_slots;
     if (call) {
         rc = splice::validate_call(*shape, call);
         if (rc != SPLICE_OK) return rc;
-        int split;
-        max_chunks = plan_chunks(*shape, *call, splice::geometry(*shape, *call), &split);
+        n_slots = splice::plan_attn(*shape, *call).n_slots;
+        if (n_slots > splice::kMaxSlots) return SPLICE_EUNSUPPORTED;
     } else {
-        max_chunks = splice::worst_default_chunks(*shape);
+        n_slots = splice::worst_default_slots(*shape);
     }
-    return (int64_t)splice::workspace_layout(*shape, max_chunks).total;
+    return (int64_t)splice::workspace_layout(*shape, n_slots).total;
 }
 
 int32_t splice_workspace_init(void *workspace, size_t workspace_bytes, void *stream) {
@@ -599,42 +1049,52 @@ int32_t splice_decode_attn(const splice_shape *shape, const splice_call *call, c
     for (const void *p : ptrs)
         if (!splice::aligned(p, 16)) return SPLICE_EINVAL;
     if (!zero && (!splice::aligned(donor_k, 16) || !splice::aligned(donor_v, 16))) return SPLICE_EINVAL;
-    if (!splice::aligned(out, 4) || !splice::aligned(lse, 4)) return SPLICE_EINVAL;
+    if (!splice::aligned(out, 16) || !splice::aligned(lse, 4)) return SPLICE_EINVAL;
 
-    const splice::Geometry geo = splice::geometry(sh, *call);
-    int split;
-    const int max_chunks = plan_chunks(sh, *call, geo, &split);
-    const splice::WorkspaceLayout wl = splice::workspace_layout(sh, max_chunks);
+    const splice::AttnPlan plan = splice::plan_attn(sh, *call);
+    if (plan.n_slots > splice::kMaxSlots) return SPLICE_EUNSUPPORTED;
+    const splice::WorkspaceLayout wl = splice::workspace_layout(sh, plan.n_slots);
     if (!workspace || !splice::aligned(workspace, 256)) return SPLICE_EWORKSPACE;
     if (workspace_bytes < wl.total) return SPLICE_EWORKSPACE;
 
     const int G = splice::group_of(sh);
-    const AttnKernels kern = pick_attn(sh.head_dim, G, sh.dtype);
-    if (!kern.attn) return SPLICE_EUNSUPPORTED;
+    const attn_fn fn = pick_attn(sh.head_dim, G, sh.dtype);
+    if (!fn) return SPLICE_EUNSUPPORTED;
 
+    const splice::Geometry &geo = plan.geo;
     AttnArgs a;
-    a.q = q;
+    a.q = (const char *)q;
     a.ck = (const char *)clean_k; a.cv = (const char *)clean_v;
     a.dk = (const char *)donor_k; a.dv = (const char *)donor_v;
     a.gk = (const char *)gen_k; a.gv = (const char *)gen_v;
     a.out = out; a.lse = lse;
+    a.counters = (int *)((char *)workspace + wl.counters_off);
     a.part = (float *)((char *)workspace + wl.part_off);
-    a.Hq = sh.n_q_heads; a.Hkv = sh.n_kv_heads; a.Tp = sh.prompt_len; a.cap = sh.gen_capacity;
-    a.step = call->step;
-    a.jp0 = geo.jp0; a.i0 = geo.i0; a.sa = geo.sa; a.sb = geo.sb; a.n_gen = geo.n_gen;
+    if (wl.part_bytes >= ((size_t)1 << 31)) return SPLICE_EUNSUPPORTED;
+    a.part_bytes = (uint32_t)(wl.part_bytes > 0 ? wl.part_bytes : 16);
+    a.C = sh.n_cells; a.Hq = sh.n_q_heads; a.Hkv = sh.n_kv_heads; a.Tp = sh.prompt_len;
+    a.cap = sh.gen_capacity;
+    a.jp0 = geo.jp0; a.i0 = geo.i0; a.n_gen = geo.n_gen; a.sa = geo.sa; a.sb = geo.sb;
     a.zero_donor = zero ? 1 : 0;
-    a.split = split;
-    a.max_chunks = max_chunks;
+    a.n_p = plan.n_p; a.p_len = plan.p_len; a.n_g = plan.n_g; a.g_len = plan.g_len;
+    a.n_slots = plan.n_slots;
     a.slot_floats = splice::slot_floats(G, sh.head_dim);
+    a.n_rb = splice::row_blocks(sh);
+    a.n_prompt_items = plan.n_prompt_items;
     a.qk_scale = call->scale * kLog2e;
     fill_mask(sh, *call, cell_LW, a.spliced);
+    // row-block order: clean cells first, then spliced cells (each by index)
+    int n = 0;
+    for (int c = 0; c < sh.n_cells; ++c)
+        if (!splice::cell_spliced(cell_LW, c, call->layer, call->step)) a.order[n++] = (uint8_t)c;
+    a.n_clean = n;
+    for (int c = 0; c < sh.n_cells; ++c)
+        if (splice::cell_spliced(cell_LW, c, call->layer, call->step)) a.order[n++] = (uint8_t)c;
+    for (; n < SPLICE_MAX_CELLS; ++n) a.order[n] = 0;
 
-    const int64_t items = (int64_t)sh.n_cells * sh.n_kv_heads * max_chunks;
+    const int64_t items = (int64_t)plan.n_prompt_items + plan.n_gen_items;
     if (items > INT32_MAX) return SPLICE_EUNSUPPORTED;
-    hipLaunchKernelGGL(kern.attn, dim3((unsigned)items), dim3(kThreads), 0, (hipStream_t)stream, a);
-    if (max_chunks > 1)
-        hipLaunchKernelGGL(kern.combine, dim3((unsigned)(sh.n_cells * sh.n_kv_heads)), dim3(kThreads), 0,
-                           (hipStream_t)stream, a);
+    hipLaunchKernelGGL(fn, dim3((unsigned)items), dim3(kThreads), 0, (hipStream_t)stream, a);
     return launch_status();
 }
 
