@@ -163,7 +163,13 @@ inline void cut(int n, int target, int split, int *k, int *len) {
     *k = ceil_div(n, *len);
 }
 
+// Prompts up to this many visible keys take the cellwise path: each (cell,
+// KV head) streams its own list, re-reading the shared prompt from L2,
+// which costs less than the row-block path's split and merge.
+constexpr int kCellwiseMaxPrompt = 512;
+
 struct AttnPlan {
+    bool cellwise;           // one work group per (cell, KV head), no merge
     Geometry geo;
     int n_p, p_len;          // prompt chunks over the visible prompt
     int n_g, g_len;          // chunks over the visible generated rows
@@ -174,6 +180,14 @@ struct AttnPlan {
 inline AttnPlan plan_attn(const splice_shape &sh, const splice_call &call) {
     AttnPlan p;
     p.geo = geometry(sh, call);
+    p.cellwise = call.split_keys == 0 && p.geo.n_prompt <= kCellwiseMaxPrompt;
+    if (p.cellwise) {
+        p.n_p = p.n_g = 0;
+        p.p_len = p.g_len = 64;
+        p.n_slots = 0;
+        p.n_prompt_items = p.n_gen_items = 0;
+        return p;
+    }
     cut(p.geo.n_prompt, prompt_chunk_target(sh), call.split_keys, &p.n_p, &p.p_len);
     cut(p.geo.n_gen, gen_chunk_target(sh), call.split_keys, &p.n_g, &p.g_len);
     p.n_slots = p.n_p + p.n_g;

@@ -73,13 +73,20 @@ __device__ __forceinline__ float dot2_bf16(uint32_t a, uint32_t b, float c) {
 // quad_perm [2,3,0,1], row_half_mirror, row_mirror.
 template <int LPK>
 __device__ __forceinline__ float group_sum(float x) {
-    x += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(x), 0xB1, 0xF, 0xF, false));
-    x += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(x), 0x4E, 0xF, 0xF, false));
+    // update_dpp with old = 0 lets the compiler fold each move into v_add_f32_dpp
+    x += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0xB1, 0xF, 0xF, false));
+    x += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x4E, 0xF, 0xF, false));
     if constexpr (LPK >= 8)
-        x += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(x), 0x141, 0xF, 0xF, false));
+        x += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x141, 0xF, 0xF, false));
     if constexpr (LPK >= 16)
-        x += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(x), 0x140, 0xF, 0xF, false));
+        x += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x140, 0xF, 0xF, false));
     return x;
+}
+
+// x + (x of the lane r places further on in its 16-lane DPP row), r in {4, 8}.
+template <int R>
+__device__ __forceinline__ float add_row_ror(float x) {
+    return x + __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x120 + R, 0xF, 0xF, false));
 }
 
 // 2^x with v_exp_f32 (results below 2^-126 flush to zero: negligible weights).
@@ -88,6 +95,17 @@ __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_ex
 __device__ __forceinline__ bool bit_set(const uint32_t *mask, int c) {
     return (mask[c >> 5] >> (c & 31)) & 1u;
 }
+
+// Compile-time loop: f(std::integral_constant<int, I>) for I in [B, E), so
+// register arrays are only ever indexed by constants.
+template <int B, int E, class F>
+__device__ __forceinline__ void static_for(F &&f) {
+    if constexpr (B < E) {
+        f(std::integral_constant<int, B>{});
+        static_for<B + 1, E>(f);
+    }
+}
+
 
 // ------------------------------------------------------------------ gather
 
@@ -189,6 +207,35 @@ __device__ __forceinline__ float part_load1(__amdgpu_buffer_rsrc_t r, uint32_t o
     return __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(r, off, 0, kSc1));
 }
 
+// ---------------------------------------------------------- vector-ALU rows
+//
+// Streams K/V rows for the G query heads of one KV head on the vector ALUs.
+// A row of D elements is cut into 16-byte pieces; LPK = D / 16 lanes share a
+// row (a "row group") and lane lj owns the NP pieces at byte offsets
+// p * LPK * 16 + lj * 16 (16 elements in all), so each load instruction of a
+// wave covers whole rows.  A row group takes U consecutive rows per
+// iteration.  q.k: v_dot2_f32_bf16 over the lane's
+// elements, then a DPP butterfly inside the row group.  The running maximum
+// of each head is wave-uniform (row groups combine with DPP, ds_swizzle and
+// readlane), so row groups never rescale against each other and the rescale
+// is a scalar branch; at the end their (l, o) are plain sums.
+template <int D, int G, bool BF16>
+struct Valu {
+    static constexpr int EB = BF16 ? 2 : 4;
+    static constexpr int EPP = 16 / EB;                        // elements per piece
+    static constexpr int LPK = D / 16;                         // lanes per row: 16 elements each
+    static constexpr int NP = EB;                              // pieces per lane
+    static constexpr int EL = 16;                              // elements per lane
+    static constexpr int KPW = 64 / LPK;                       // row groups per wave
+    static constexpr int RGR = 16 / LPK;                       // row groups per 16-lane DPP row
+    static constexpr int ROW = D * EB;
+    static constexpr int PSTRIDE = LPK * 16;
+    static constexpr int U = 4;
+    static constexpr int QW = NP * 4;                          // q dwords per head per lane
+    // element index of piece p, element e of lane lj
+    static __device__ __forceinline__ int elem(int lj, int p, int e) { return p * LPK * EPP + lj * EPP + e; }
+};
+
 // LDS budget of one work group.
 template <int D, int G, bool BF16>
 struct Lds {
@@ -196,201 +243,170 @@ struct Lds {
     static constexpr int KROW = D * 2 + 16;        // K tile row stride (bytes), padded
     static constexpr int VROW = KT * 2 + 8;        // V^T tile row stride (bytes), padded
     static constexpr int TILES = BF16 ? KT * KROW + D * VROW : 0;
-    static constexpr int MERGE = kWaves * G * (D + 2) * 4;
+    static constexpr int MERGE = kWaves * 4 * G * (D + 1) * 4 + kWaves * G * 4;
     static constexpr int STAGE = 2 * kMaxSlots * kRowBlock * 4;
     static constexpr int BYTES = TILES > MERGE ? (TILES > STAGE ? TILES : STAGE)
                                                : (MERGE > STAGE ? MERGE : STAGE);
 };
 
-// ---------------------------------------------------------- vector-ALU rows
-//
-// Streams K/V rows [kbeg, kend) for the G query heads of one KV head.
-// Lane layout for a row of D elements of EB bytes: LPK = D / 16 lanes per
-// row (a "row group"), KPW = 64 / LPK row groups per wave; lane lj owns
-// NP = EB pieces of 16 bytes at byte offsets p * (D * EB / NP) + lj * 16, so
-// each load instruction of a wave covers KPW rows x D bytes without gaps.
-// A row group takes U consecutive rows per iteration and keeps its own
-// online-softmax state; row groups and waves are merged at the end.
-template <int D, int G, bool BF16>
-struct Valu {
-    static constexpr int EB = BF16 ? 2 : 4;
-    static constexpr int LPK = D / 16;
-    static constexpr int KPW = 64 / LPK;
-    static constexpr int NP = EB;
-    static constexpr int EPP = 16 / EB;
-    static constexpr int PIECE = D * EB / NP;
-    static constexpr int ROW = D * EB;
-    static constexpr int U = (BF16 && G <= 4) ? 4 : 2;
-    static constexpr int QW = BF16 ? 8 : 16;
-};
+// Maximum over the row groups of a wave of a value that is the same in all
+// lanes of a row group; the result is wave-uniform.
+template <int LPK>
+__device__ __forceinline__ float wave_max_rows(float x) {
+    // row groups of a 16-lane DPP row (rotations keep a max all-reduce exact)
+    if constexpr (LPK <= 4)
+        x = fmaxf(x, __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x124, 0xF, 0xF, false)));
+    if constexpr (LPK <= 8)
+        x = fmaxf(x, __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x128, 0xF, 0xF, false)));
+    x = fmaxf(x, __int_as_float(__builtin_amdgcn_ds_swizzle(__float_as_int(x), 0x401F)));   // lane ^ 16
+    return fmaxf(__int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), 0)),
+                 __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), 32)));
+}
 
 template <int D, int G, bool BF16>
 __device__ __forceinline__ void load_q(const AttnArgs &a, int c, int g, uint32_t (&qr)[G][Valu<D, G, BF16>::QW]) {
     using V = Valu<D, G, BF16>;
     const int lj = (threadIdx.x & 63) % V::LPK;
     const char *qb = a.q + ((size_t)c * a.Hq + (size_t)g * G) * V::ROW;
-#pragma unroll
-    for (int h = 0; h < G; ++h)
-#pragma unroll
-        for (int p = 0; p < V::NP; ++p) {
-            const uint4 w = *reinterpret_cast<const uint4 *>(qb + (size_t)h * V::ROW + p * V::PIECE + lj * 16);
-            qr[h][p * 4 + 0] = w.x;
-            qr[h][p * 4 + 1] = w.y;
-            qr[h][p * 4 + 2] = w.z;
-            qr[h][p * 4 + 3] = w.w;
-        }
+    static_for<0, G>([&](auto h) {
+        static_for<0, V::NP>([&](auto p) {
+            const u32x4_t w = *reinterpret_cast<const u32x4_t *>(qb + (size_t)h * V::ROW + p * V::PSTRIDE + lj * 16);
+            static_for<0, 4>([&](auto i) { qr[h][p * 4 + i] = w[(int)i]; });
+        });
+    });
 }
 
 // row_of(key, &k_row, &v_row) -> false if the key is not to be attended
-// (its pointers must still be readable).
+// (its pointers must still be readable).  m is wave-uniform on return.
 template <int D, int G, bool BF16, class RowFn>
 __device__ __forceinline__ void valu_stream(const uint32_t (&qr)[G][Valu<D, G, BF16>::QW], int kbeg, int kend,
-                                            float qk_scale, RowFn row_of,
-                                            float (&m)[G], float (&l)[G], float (&o)[G][16]) {
+                                            float qk_scale, RowFn row_of, float (&m)[G], float (&l)[G],
+                                            float (&o)[G][Valu<D, G, BF16>::EL]) {
     using V = Valu<D, G, BF16>;
     constexpr int U = V::U;
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int lj = lane % V::LPK, rg = lane / V::LPK;
-#pragma unroll
-    for (int h = 0; h < G; ++h) {
+    static_for<0, G>([&](auto h) {
         m[h] = -INFINITY;
         l[h] = 0.f;
-#pragma unroll
-        for (int e = 0; e < 16; ++e) o[h][e] = 0.f;
-    }
+        static_for<0, V::EL>([&](auto e) { o[h][e] = 0.f; });
+    });
     for (int base = kbeg + wave * (V::KPW * U); base < kend; base += kWaves * V::KPW * U) {
         const int kf = base + rg * U;
-        uint4 kr[U][V::NP], vr[U][V::NP];
+        u32x4_t kr[U][V::NP], vr[U][V::NP];
         bool ok[U];
-#pragma unroll
-        for (int u = 0; u < U; ++u) {
+        static_for<0, U>([&](auto u) {
             const int key = kf + u;
             const bool inr = key < kend;
             const char *kp;
             const char *vp;
             const bool use = row_of(inr ? key : kend - 1, kp, vp);
             ok[u] = inr && use;
-#pragma unroll
-            for (int p = 0; p < V::NP; ++p) {
-                kr[u][p] = *reinterpret_cast<const uint4 *>(kp + p * V::PIECE + lj * 16);
-                vr[u][p] = *reinterpret_cast<const uint4 *>(vp + p * V::PIECE + lj * 16);
-            }
-        }
+            static_for<0, V::NP>([&](auto p) {
+                kr[u][p] = *reinterpret_cast<const u32x4_t *>(kp + p * V::PSTRIDE + lj * 16);
+                vr[u][p] = *reinterpret_cast<const u32x4_t *>(vp + p * V::PSTRIDE + lj * 16);
+            });
+        });
         float s[U][G];
-#pragma unroll
-        for (int u = 0; u < U; ++u)
-#pragma unroll
-            for (int h = 0; h < G; ++h) {
+        static_for<0, U>([&](auto u) {
+            static_for<0, G>([&](auto h) {
                 float acc = 0.f;
-#pragma unroll
-                for (int p = 0; p < V::NP; ++p) {
-                    const uint32_t kw[4] = {kr[u][p].x, kr[u][p].y, kr[u][p].z, kr[u][p].w};
-#pragma unroll
-                    for (int i = 0; i < 4; ++i) {
+                static_for<0, V::NP>([&](auto p) {
+                    static_for<0, 4>([&](auto i) {
                         if constexpr (BF16)
-                            acc = dot2_bf16(qr[h][p * 4 + i], kw[i], acc);
+                            acc = dot2_bf16(qr[h][p * 4 + i], kr[u][p][(int)i], acc);
                         else
-                            acc = fmaf(__uint_as_float(qr[h][p * 4 + i]), __uint_as_float(kw[i]), acc);
-                    }
-                }
+                            acc = fmaf(__uint_as_float(qr[h][p * 4 + i]), __uint_as_float(kr[u][p][(int)i]), acc);
+                    });
+                });
                 acc = group_sum<V::LPK>(acc) * qk_scale;
                 s[u][h] = ok[u] ? acc : -INFINITY;
-            }
-        float vf[U][16];
-#pragma unroll
-        for (int u = 0; u < U; ++u)
-#pragma unroll
-            for (int p = 0; p < V::NP; ++p) {
-                const uint32_t vw[4] = {vr[u][p].x, vr[u][p].y, vr[u][p].z, vr[u][p].w};
-#pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    if constexpr (BF16) {
-                        vf[u][p * V::EPP + 2 * i] = bf16_lo(vw[i]);
-                        vf[u][p * V::EPP + 2 * i + 1] = bf16_hi(vw[i]);
-                    } else {
-                        vf[u][p * V::EPP + i] = __uint_as_float(vw[i]);
-                    }
-                }
-            }
+            });
+        });
         float mt[G];
         bool need = false;
-#pragma unroll
-        for (int h = 0; h < G; ++h) {
-            mt[h] = s[0][h];
-#pragma unroll
-            for (int u = 1; u < U; ++u) mt[h] = fmaxf(mt[h], s[u][h]);
+        static_for<0, G>([&](auto h) {
+            float x = s[0][h];
+            static_for<1, U>([&](auto u) { x = fmaxf(x, s[u][h]); });
+            mt[h] = wave_max_rows<V::LPK>(x);
             need |= mt[h] > m[h] + kSlack;
-        }
-        if (__any(need)) {
-#pragma unroll
-            for (int h = 0; h < G; ++h) {
-                const bool nh = mt[h] > m[h] + kSlack;
-                const float mn = nh ? fmaxf(m[h], mt[h]) : m[h];
-                const float al = nh ? fast_exp2(m[h] - (mn == -INFINITY ? 0.f : mn)) : 1.f;
+        });
+        if (need) {   // wave-uniform
+            static_for<0, G>([&](auto h) {
+                const float mn = fmaxf(m[h], mt[h]);
+                const float al = fast_exp2(m[h] - (mn == -INFINITY ? 0.f : mn));
                 l[h] *= al;
-#pragma unroll
-                for (int e = 0; e < 16; ++e) o[h][e] *= al;
+                static_for<0, V::EL>([&](auto e) { o[h][e] *= al; });
                 m[h] = mn;
-            }
+            });
         }
-#pragma unroll
-        for (int h = 0; h < G; ++h) {
+        float pw[U][G];
+        static_for<0, G>([&](auto h) {
             const float ms = m[h] == -INFINITY ? 0.f : m[h];
-#pragma unroll
-            for (int u = 0; u < U; ++u) {
-                const float pw = fast_exp2(s[u][h] - ms);
-                l[h] += pw;
-#pragma unroll
-                for (int e = 0; e < 16; ++e) o[h][e] = fmaf(pw, vf[u][e], o[h][e]);
-            }
-        }
+            static_for<0, U>([&](auto u) {
+                pw[u][h] = fast_exp2(s[u][h] - ms);
+                l[h] += pw[u][h];
+            });
+        });
+        static_for<0, U>([&](auto u) {
+            static_for<0, V::NP>([&](auto p) {
+                static_for<0, 4>([&](auto i) {
+                    constexpr int pp = decltype(p)::value, ii = decltype(i)::value;
+                    if constexpr (BF16) {
+                        const float v0 = bf16_lo(vr[u][p][ii]), v1 = bf16_hi(vr[u][p][ii]);
+                        static_for<0, G>([&](auto h) {
+                            o[h][pp * 8 + 2 * ii] = fmaf(pw[u][h], v0, o[h][pp * 8 + 2 * ii]);
+                            o[h][pp * 8 + 2 * ii + 1] = fmaf(pw[u][h], v1, o[h][pp * 8 + 2 * ii + 1]);
+                        });
+                    } else {
+                        const float v0 = __uint_as_float(vr[u][p][ii]);
+                        static_for<0, G>([&](auto h) { o[h][pp * 4 + ii] = fmaf(pw[u][h], v0, o[h][pp * 4 + ii]); });
+                    }
+                });
+            });
+        });
     }
 }
 
-// Merge the row groups of each wave (lane butterfly) and the waves (LDS),
-// then store the work item's partial result into `slot` with agent-scope
-// stores: o[G][D], m[G], l[G].
-template <int D, int G, bool BF16>
-__device__ __forceinline__ void valu_store_partial(const AttnArgs &a, float (&m)[G], float (&l)[G], float (&o)[G][16],
-                                                   char *buf, uint32_t slot) {
+// Sum the row groups (same maximum within a wave) and merge the waves
+// (LDS); sink(h, d, M, L, O) receives four consecutive outputs of head h.
+template <int D, int G, bool BF16, typename StoreFn, int EL = Valu<D, G, BF16>::EL>
+__device__ __forceinline__ void valu_merge(float (&m)[G], float (&l)[G], float (&o)[G][EL],
+                                           char *buf, StoreFn sink) {
     using V = Valu<D, G, BF16>;
-    float *s_o = reinterpret_cast<float *>(buf);              // [kWaves][G][D]
-    float *s_m = s_o + kWaves * G * D;                         // [kWaves][G]
-    float *s_l = s_m + kWaves * G;                             // [kWaves][G]
+    float *s_o = reinterpret_cast<float *>(buf);              // [kWaves][4][G][D]
+    float *s_l = s_o + kWaves * 4 * G * D;                     // [kWaves][4][G]
+    float *s_m = s_l + kWaves * 4 * G;                         // [kWaves][G]
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int lj = lane % V::LPK, rg = lane / V::LPK;
-#pragma unroll
-    for (int off = V::LPK; off < 64; off <<= 1) {
-#pragma unroll
-        for (int h = 0; h < G; ++h) {
-            const float mo = __shfl_xor(m[h], off);
-            const float lo = __shfl_xor(l[h], off);
-            const float mx = fmaxf(m[h], mo);
-            const float ms = mx == -INFINITY ? 0.f : mx;
-            const float fa = fast_exp2(m[h] - ms), fb = fast_exp2(mo - ms);
-            l[h] = l[h] * fa + lo * fb;
-#pragma unroll
-            for (int e = 0; e < 16; ++e) o[h][e] = o[h][e] * fa + __shfl_xor(o[h][e], off) * fb;
-            m[h] = mx;
-        }
-    }
+    const int drow = lane >> 4;                                // 16-lane DPP row of this lane
+    // sum the row groups that share a DPP row (same maximum: plain sums)
+    static_for<0, G>([&](auto h) {
+        if constexpr (V::RGR >= 4) l[h] = add_row_ror<4>(l[h]);
+        if constexpr (V::RGR >= 2) l[h] = add_row_ror<8>(l[h]);
+        static_for<0, V::EL>([&](auto e) {
+            if constexpr (V::RGR >= 4) o[h][e] = add_row_ror<4>(o[h][e]);
+            if constexpr (V::RGR >= 2) o[h][e] = add_row_ror<8>(o[h][e]);
+        });
+    });
     __syncthreads();   // buf may still be read by a previous phase
-    if (rg == 0) {
-#pragma unroll
-        for (int h = 0; h < G; ++h) {
-#pragma unroll
-            for (int p = 0; p < V::NP; ++p)
-#pragma unroll
-                for (int i = 0; i < V::EPP; ++i)
-                    s_o[(wave * G + h) * D + p * (D / V::NP) + lj * V::EPP + i] = o[h][p * V::EPP + i];
-            if (lj == 0) {
-                s_m[wave * G + h] = m[h];
-                s_l[wave * G + h] = l[h];
-            }
-        }
+    if (rg % V::RGR == 0) {   // the first row group of each DPP row holds its sum
+        static_for<0, G>([&](auto h) {
+            float *dst = s_o + ((wave * 4 + drow) * G + h) * D;
+            static_for<0, V::NP>([&](auto p) {
+                constexpr int pp = decltype(p)::value;
+                static_for<0, V::EPP / 4>([&](auto q4) {
+                    constexpr int qq = decltype(q4)::value;
+                    *reinterpret_cast<f32x4_t *>(dst + V::elem(lj, pp, 4 * qq)) =
+                        f32x4_t{o[h][pp * V::EPP + 4 * qq + 0], o[h][pp * V::EPP + 4 * qq + 1],
+                                o[h][pp * V::EPP + 4 * qq + 2], o[h][pp * V::EPP + 4 * qq + 3]};
+                });
+            });
+            if (lj == 0) s_l[(wave * 4 + drow) * G + h] = l[h];
+        });
     }
+    if (lane == 0) static_for<0, G>([&](auto h) { s_m[wave * G + h] = m[h]; });
     __syncthreads();
-    const __amdgpu_buffer_rsrc_t r = part_rsrc(a);
     for (int e = tid; e < G * D / 4; e += kThreads) {   // four consecutive d per thread
         const int h = e / (D / 4), d = 4 * (e % (D / 4));
         float M = -INFINITY;
@@ -402,15 +418,33 @@ __device__ __forceinline__ void valu_store_partial(const AttnArgs &a, float (&m)
 #pragma unroll
         for (int w = 0; w < kWaves; ++w) {
             const float f = fast_exp2(s_m[w * G + h] - Ms);
-            L = fmaf(s_l[w * G + h], f, L);
-            O += *reinterpret_cast<const f32x4_t *>(s_o + (w * G + h) * D + d) * f;
+            float lw = 0.f;
+            f32x4_t ow = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int r4 = 0; r4 < 4; ++r4) {
+                lw += s_l[(w * 4 + r4) * G + h];
+                ow += *reinterpret_cast<const f32x4_t *>(s_o + ((w * 4 + r4) * G + h) * D + d);
+            }
+            L = fmaf(lw, f, L);
+            O += ow * f;
         }
+        sink(h, d, M, L, O);
+    }
+}
+
+// Store the merged state as the item's partial result (sc1 stores):
+// o[G][D], m[G], l[G].
+template <int D, int G, bool BF16>
+__device__ __forceinline__ void valu_store_partial(const AttnArgs &a, float (&m)[G], float (&l)[G],
+                                                   float (&o)[G][Valu<D, G, BF16>::EL], char *buf, uint32_t slot) {
+    const __amdgpu_buffer_rsrc_t r = part_rsrc(a);
+    valu_merge<D, G, BF16>(m, l, o, buf, [&](int h, int d, float M, float L, f32x4_t O) {
         part_store4(r, slot + (uint32_t)(h * D + d) * 4u, O);
         if (d == 0) {
             part_store1(r, slot + (uint32_t)(G * D + h) * 4u, M);
             part_store1(r, slot + (uint32_t)(G * D + G + h) * 4u, L);
         }
-    }
+    });
 }
 
 // Byte offset of slot k of (cell c, KV head g) in the partial region.
@@ -428,7 +462,7 @@ __device__ void gen_item(const AttnArgs &a, int c, int g, int gk, char *buf) {
     const int r1 = min(r0 + a.g_len, a.i0 + a.n_gen);
     const size_t off = ((size_t)c * a.Hkv + g) * (size_t)a.cap * V::ROW;
     const char *kb = a.gk + off, *vb = a.gv + off;
-    float m[G], l[G], o[G][16];
+    float m[G], l[G], o[G][V::EL];
     valu_stream<D, G, BF16>(qr, r0, r1, a.qk_scale,
                             [&](int key, const char *&kp, const char *&vp) {
                                 kp = kb + (size_t)key * V::ROW;
@@ -451,7 +485,7 @@ __device__ void prompt_item_valu(const AttnArgs &a, int c, int g, int pk, char *
     const int k1 = min(k0 + a.p_len, a.Tp);
     const bool spl = bit_set(a.spliced, c);
     const size_t head = (size_t)g * a.Tp * V::ROW;
-    float m[G], l[G], o[G][16];
+    float m[G], l[G], o[G][V::EL];
     valu_stream<D, G, BF16>(qr, k0, k1, a.qk_scale,
                             [&](int j, const char *&kp, const char *&vp) {
                                 const bool in_span = j >= a.sa && j < a.sb;
@@ -464,25 +498,6 @@ __device__ void prompt_item_valu(const AttnArgs &a, int c, int g, int pk, char *
                             m, l, o);
     valu_store_partial<D, G, BF16>(a, m, l, o, buf, slot_off(a, c, g, pk));
 }
-
-// ------------------------------------------------------- MFMA prompt rows
-//
-// One prompt chunk [k0, k1) for kRowBlock = 64 rows of one KV head; wave w
-// owns rows 16w..16w+15, lane (col = l % 16, quad = l / 16) owns row col.
-// Per tile of 64 keys (and per source: clean pass, then donor pass when the
-// block has spliced rows and the tile touches the span):
-//   * K rows and the transposed V tile are staged in LDS once, for all rows;
-//   * S^T (keys x rows) = K Q^T with v_mfma_f32_16x16x32_bf16 (A = K from
-//     LDS, B = this lane's q fragment); lane holds keys 16 sub + 4 quad + i;
-//   * masks: key in the chunk, and the key belongs to this pass for this
-//     row (non-span keys and the span of clean rows read clean; the span of
-//     spliced rows reads the donor; ZERO rows skip the span);
-//   * online softmax with a shared row maximum (4 quads), lazy rescale;
-//   * O^T (d x rows) += V^T P^T, P split into bf16 hi + lo parts so the
-//     weights keep ~16 significant bits.  Lane holds O^T[16 dt + 4 quad + i]
-//     for its own row, so the rescale by the row's factor is lane-local.
-typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
-typedef float f32x4_t __attribute__((ext_vector_type(4)));
 
 // One thread's share of staging a KT-key prompt tile: K in 16-byte units
 // (row-major in LDS), V in units of 4 keys x 8 d (transposed in LDS, so the
@@ -497,16 +512,6 @@ struct TileIo {
     static constexpr int NKU = KUNITS / kThreads;
     static constexpr int NVU = VUNITS >= kThreads ? VUNITS / kThreads : 1;
 };
-
-// Compile-time loop: f(std::integral_constant<int, I>) for I in [B, E), so
-// register arrays are only ever indexed by constants.
-template <int B, int E, class F>
-__device__ __forceinline__ void static_for(F &&f) {
-    if constexpr (B < E) {
-        f(std::integral_constant<int, B>{});
-        static_for<B + 1, E>(f);
-    }
-}
 
 template <int D>
 __device__ __forceinline__ void tile_fetch(u32x4_t (&kreg)[TileIo<D>::NKU], u32x4_t (&vreg)[TileIo<D>::NVU][4],
@@ -885,6 +890,63 @@ __global__ __launch_bounds__(kThreads) void attn_kernel(AttnArgs a) {
     }
 }
 
+// ------------------------------------------------------- cellwise kernel
+//
+// Short prompts: one work group per (cell, KV head) streams the cell's
+// whole visible list -- prompt slots read from the clean or the donor cache
+// by pointer (a ZERO cell skips its span), then its generated rows -- and
+// writes out and lse itself.  No partial results and no merge; the prompt
+// tiles the cells share are re-read from L2.  Chosen by the host when the
+// prompt is short enough for that to be cheaper than the row-block path.
+template <int D, int G, bool BF16>
+__global__ __launch_bounds__(kThreads) void cellwise_kernel(AttnArgs a) {
+    using V = Valu<D, G, BF16>;
+    __shared__ __attribute__((aligned(16))) char buf[kWaves * 4 * G * (D + 1) * 4 + kWaves * G * 4];
+    const int g = blockIdx.x % a.Hkv;
+    const int c = blockIdx.x / a.Hkv;
+    uint32_t qr[G][V::QW];
+    load_q<D, G, BF16>(a, c, g, qr);
+    const bool spl = bit_set(a.spliced, c);
+    const bool zskip = spl && a.zero_donor;
+    const int nsv = a.sb - a.sa;
+    const int n_pl = (a.Tp - a.jp0) - (zskip ? nsv : 0);   // prompt part of the list
+    const int n_list = n_pl + a.n_gen;
+    const size_t head = (size_t)g * a.Tp * V::ROW;
+    const char *gkb = a.gk + ((size_t)c * a.Hkv + g) * (size_t)a.cap * V::ROW;
+    const char *gvb = a.gv + ((size_t)c * a.Hkv + g) * (size_t)a.cap * V::ROW;
+    float m[G], l[G], o[G][V::EL];
+    valu_stream<D, G, BF16>(qr, 0, n_list, a.qk_scale,
+                            [&](int v, const char *&kp, const char *&vp) {
+                                if (v < n_pl) {
+                                    int j = a.jp0 + v;
+                                    if (zskip && j >= a.sa) j += nsv;
+                                    const bool donor = spl && !a.zero_donor && j >= a.sa && j < a.sb;
+                                    const size_t off = head + (size_t)j * V::ROW;
+                                    kp = (donor ? a.dk : a.ck) + off;
+                                    vp = (donor ? a.dv : a.cv) + off;
+                                } else {
+                                    const size_t off = (size_t)(a.i0 + (v - n_pl)) * V::ROW;
+                                    kp = gkb + off;
+                                    vp = gvb + off;
+                                }
+                                return true;
+                            },
+                            m, l, o);
+    const bool zero_term = zskip && nsv > 0;
+    valu_merge<D, G, BF16>(m, l, o, buf, [&](int h, int d, float M, float L, f32x4_t O) {
+        if (zero_term) {   // nsv keys of score 0 and value 0
+            const float Mz = fmaxf(M, 0.f);
+            const float f = fast_exp2(M - Mz);
+            L = L * f + (float)nsv * fast_exp2(-Mz);
+            O *= f;
+            M = Mz;
+        }
+        const int row = c * a.Hq + g * G + h;
+        *reinterpret_cast<f32x4_t *>(a.out + (size_t)row * D + d) = O * (1.f / L);
+        if (d == 0) a.lse[row] = (M + log2f(L)) * kLn2;
+    });
+}
+
 __global__ __launch_bounds__(kThreads) void fill_kernel(uint32_t *p, size_t n_words) {
     for (size_t i = (size_t)blockIdx.x * kThreads + threadIdx.x; i < n_words;
          i += (size_t)gridDim.x * kThreads)
@@ -894,29 +956,37 @@ __global__ __launch_bounds__(kThreads) void fill_kernel(uint32_t *p, size_t n_wo
 // ------------------------------------------------------------ dispatch
 
 typedef void (*attn_fn)(AttnArgs);
+struct AttnKernels {
+    attn_fn rowblock, cellwise;
+};
+
+template <int D, int G, bool BF16>
+AttnKernels kernels_of() {
+    return AttnKernels{attn_kernel<D, G, BF16>, cellwise_kernel<D, G, BF16>};
+}
 
 template <int D, bool BF16>
-attn_fn pick_g(int G) {
+AttnKernels pick_g(int G) {
     switch (G) {
-    case 1: return attn_kernel<D, 1, BF16>;
-    case 2: return attn_kernel<D, 2, BF16>;
-    case 4: return attn_kernel<D, 4, BF16>;
-    case 8: return attn_kernel<D, 8, BF16>;
-    default: return nullptr;
+    case 1: return kernels_of<D, 1, BF16>();
+    case 2: return kernels_of<D, 2, BF16>();
+    case 4: return kernels_of<D, 4, BF16>();
+    case 8: return kernels_of<D, 8, BF16>();
+    default: return AttnKernels{nullptr, nullptr};
     }
 }
 
 template <bool BF16>
-attn_fn pick_d(int D, int G) {
+AttnKernels pick_d(int D, int G) {
     switch (D) {
     case 64: return pick_g<64, BF16>(G);
     case 128: return pick_g<128, BF16>(G);
     case 256: return pick_g<256, BF16>(G);
-    default: return nullptr;
+    default: return AttnKernels{nullptr, nullptr};
     }
 }
 
-attn_fn pick_attn(int D, int G, int dtype) {
+AttnKernels pick_attn(int D, int G, int dtype) {
     return dtype == SPLICE_BF16 ? pick_d<true>(D, G) : pick_d<false>(D, G);
 }
 
@@ -1058,8 +1128,8 @@ int32_t splice_decode_attn(const splice_shape *shape, const splice_call *call, c
     if (workspace_bytes < wl.total) return SPLICE_EWORKSPACE;
 
     const int G = splice::group_of(sh);
-    const attn_fn fn = pick_attn(sh.head_dim, G, sh.dtype);
-    if (!fn) return SPLICE_EUNSUPPORTED;
+    const AttnKernels kern = pick_attn(sh.head_dim, G, sh.dtype);
+    if (!kern.rowblock) return SPLICE_EUNSUPPORTED;
 
     const splice::Geometry &geo = plan.geo;
     AttnArgs a;
@@ -1092,9 +1162,14 @@ int32_t splice_decode_attn(const splice_shape *shape, const splice_call *call, c
         if (splice::cell_spliced(cell_LW, c, call->layer, call->step)) a.order[n++] = (uint8_t)c;
     for (; n < SPLICE_MAX_CELLS; ++n) a.order[n] = 0;
 
+    if (plan.cellwise) {
+        hipLaunchKernelGGL(kern.cellwise, dim3((unsigned)(sh.n_cells * sh.n_kv_heads)), dim3(kThreads), 0,
+                           (hipStream_t)stream, a);
+        return launch_status();
+    }
     const int64_t items = (int64_t)plan.n_prompt_items + plan.n_gen_items;
     if (items > INT32_MAX) return SPLICE_EUNSUPPORTED;
-    hipLaunchKernelGGL(fn, dim3((unsigned)items), dim3(kThreads), 0, (hipStream_t)stream, a);
+    hipLaunchKernelGGL(kern.rowblock, dim3((unsigned)items), dim3(kThreads), 0, (hipStream_t)stream, a);
     return launch_status();
 }
 
