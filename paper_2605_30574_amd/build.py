@@ -1,28 +1,38 @@
 """Build the gfx950 splice library in-tree: paper_2605_30574_amd/libsplice_attn.so.
 
     python -m paper_2605_30574_amd.build
+
+Each translation unit under csrc/ (the host/ABI unit and one unit per
+(head_dim, element type) of the attention kernels) is compiled to an object
+in parallel, then the objects are linked into one shared library.
 """
 from __future__ import annotations
 
+import glob
 import os
 import shutil
 import subprocess
 import sys
+from concurrent.futures import ThreadPoolExecutor
 
 PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 INCLUDE = os.path.join(ROOT, "include")
 CSRC = os.path.join(PKG, "csrc")
-SOURCES = [os.path.join(CSRC, "splice_attn.hip")]
+OBJDIR = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libsplice_attn.so")
 ARCH = "gfx950"
 
-HIPCC_FLAGS = [
-    f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC", "-shared",
-    "-fvisibility=hidden", "-Wall",
+COMPILE_FLAGS = [
+    f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC", "-fvisibility=hidden", "-Wall",
     # no packed-FP32 instructions in device code
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
 ]
+NOISE = "is not a recognized feature for this target"
+
+
+def sources():
+    return sorted(glob.glob(os.path.join(CSRC, "*.hip")))
 
 
 def hipcc() -> str:
@@ -32,20 +42,40 @@ def hipcc() -> str:
     raise RuntimeError("hipcc not found: the splice library needs ROCm's hipcc")
 
 
-def build(out: str = LIB, extra=(), verbose: bool = False) -> str:
-    cmd = [hipcc(), *HIPCC_FLAGS, f"-I{INCLUDE}", f"-I{CSRC}", *extra, "-o", out + ".tmp", *SOURCES]
-    if verbose:
-        print(" ".join(cmd), flush=True)
+def _run(cmd):
     res = subprocess.run(cmd, capture_output=True, text=True)
-    noise = "is not a recognized feature for this target"
-    msgs = [ln for ln in (res.stderr or "").splitlines() if noise not in ln]
-    if res.returncode != 0:
-        raise RuntimeError("hipcc failed:\n" + "\n".join(msgs))
-    if verbose and msgs:
-        print("\n".join(msgs), file=sys.stderr)
+    msgs = [ln for ln in (res.stderr or "").splitlines() if NOISE not in ln]
+    return res.returncode, msgs
+
+
+def build(out: str = LIB, extra=(), verbose: bool = False, jobs: int = 0) -> str:
+    cc = hipcc()
+    os.makedirs(OBJDIR, exist_ok=True)
+    srcs = sources()
+    objs = [os.path.join(OBJDIR, os.path.basename(s)[:-4] + ".o") for s in srcs]
+    cmds = [[cc, *COMPILE_FLAGS, f"-I{INCLUDE}", f"-I{CSRC}", *extra, "-c", "-o", o, s]
+            for s, o in zip(srcs, objs)]
+    jobs = jobs or min(len(cmds), max(1, min(16, os.cpu_count() or 1)))
+    if verbose:
+        for c in cmds:
+            print(" ".join(c), flush=True)
+    with ThreadPoolExecutor(max_workers=jobs) as ex:
+        results = list(ex.map(_run, cmds))
+    failed = [(c, m) for c, (rc, m) in zip(cmds, results) if rc != 0]
+    if failed:
+        raise RuntimeError("hipcc failed:\n" + "\n".join(
+            " ".join(c[-1:]) + "\n" + "\n".join(m) for c, m in failed))
+    if verbose:
+        for _, m in results:
+            if m:
+                print("\n".join(m), file=sys.stderr)
+    link = [cc, f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", out + ".tmp", *objs]
+    rc, msgs = _run(link)
+    if rc != 0:
+        raise RuntimeError("link failed:\n" + "\n".join(msgs))
     os.replace(out + ".tmp", out)
     return out
 
 
 if __name__ == "__main__":
-    print(build(verbose=True))
+    print(build(verbose="-v" in sys.argv))

@@ -1,0 +1,6 @@
+// Instantiates the attention kernels for head_dim 128, bf16 inputs.
+#include "attn_kernels.hpp"
+
+namespace splice_dev {
+AttnKernels attn_kernels_d128_bf16(int G) { return pick_g<128, true>(G); }
+}  // namespace splice_dev
