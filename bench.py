@@ -38,8 +38,9 @@ sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
 PROFILES = os.path.join(ROOT, "profiles")
-KERNEL_SOURCES = [os.path.join(ROOT, "paper_2605_30574_amd", "csrc", f)
-                  for f in ("splice_attn.hip", "plan.hpp")]
+CSRC = os.path.join(ROOT, "paper_2605_30574_amd", "csrc")
+KERNEL_SOURCES = sorted(os.path.join(CSRC, f) for f in os.listdir(CSRC)
+                        if f.endswith((".hip", ".hpp")))
 
 
 def log(msg: str) -> None:
