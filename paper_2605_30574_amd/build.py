@@ -27,6 +27,10 @@ COMPILE_FLAGS = [
     f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC", "-fvisibility=hidden", "-Wall",
     # no packed-FP32 instructions in device code
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    # MFMA sources and results in VGPRs: the accumulators stay where the
+    # online-softmax rescale (a vector-ALU multiply) can reach them, with no
+    # AGPR copies in the streaming loops
+    "-mllvm", "-amdgpu-mfma-vgpr-form",
 ]
 NOISE = "is not a recognized feature for this target"
 

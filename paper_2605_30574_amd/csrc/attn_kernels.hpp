@@ -5,6 +5,7 @@
 #pragma once
 
 #include "device_common.hpp"
+#include "prompt_wide.hpp"
 #include "wave_mfma.hpp"
 
 namespace splice_dev {
@@ -22,6 +23,7 @@ struct AttnArgs {
     int zero_donor;
     int n_p, p_len, n_g, g_len, n_slots, slot_floats;
     int n_rb, n_prompt_items, n_clean;
+    int n_rg_clean;   // bf16 prompt row groups of unspliced cells (the rest: spliced cells)
     float qk_scale;   // scale * log2(e)
     uint32_t spliced[SPLICE_MAX_CELLS / 32];
     uint8_t order[SPLICE_MAX_CELLS];   // clean cells, then spliced cells
@@ -82,21 +84,17 @@ struct Valu {
 };
 
 // LDS budget of one work group.
+// LDS of the f32 items kernel: row-group sums of the vector-ALU stream and
+// the merge staging.
 template <int D, int G, bool BF16>
 struct Lds {
-    static constexpr int KT = 64;                  // keys per staged prompt tile
-    static constexpr int KROW = D * 2 + 16;        // K tile row stride (bytes), padded
-    static constexpr int VROW = KT * 2 + 8;        // V^T tile row stride (bytes), padded
-    static constexpr int TILES = BF16 ? KT * KROW + D * VROW : 0;
     static constexpr int MERGE = kWaves * 4 * G * (D + 1) * 4 + kWaves * G * 4;
     static constexpr int STAGE = 2 * kMaxSlots * kRowBlock * 4;
-    // bf16 generated-row items: one V^T tile per wave, then the wave merge
-    static constexpr int GEN_TILES = BF16 ? kWaves * WaveMfma<D>::LDS : 0;
-    static constexpr int GEN_MERGE = BF16 ? kWaves * G * (D + 2) * 4 : 0;
-    static constexpr int BYTES = cmax(cmax(TILES, MERGE), cmax(STAGE, cmax(GEN_TILES, GEN_MERGE)));
+    static constexpr int BYTES = cmax(MERGE, STAGE);
 };
 
-// LDS of the bf16 cellwise kernel.
+// LDS of the bf16 per-(cell, KV head) kernels: one V^T tile per wave, then
+// the wave merge.
 template <int D, int G>
 struct CellwiseLds {
     static constexpr int BYTES = cmax(kWaves * WaveMfma<D>::LDS, kWaves * G * (D + 2) * 4);
@@ -326,35 +324,6 @@ __device__ void gen_item(const AttnArgs &a, int c, int g, int gk, char *buf) {
     valu_store_partial<D, G, BF16>(a, m, l, o, buf, slot_off(a, c, g, a.n_p + gk));
 }
 
-// Generated rows of one (cell, KV head) on the matrix cores (bf16): the four
-// waves take interleaved 32-row tiles of the chunk and merge in LDS.
-template <int D, int G>
-__device__ void gen_item_mfma(const AttnArgs &a, int c, int g, int gk, char *buf) {
-    using W = WaveMfma<D>;
-    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);   // uniform: tile pointers stay scalar
-    bf16x8_t qb[W::NDS];
-    load_q_mfma<D, G>(a.q + ((size_t)c * a.Hq + (size_t)g * G) * W::ROW, qb);
-    const int r0 = a.i0 + gk * a.g_len;
-    const int r1 = min(r0 + a.g_len, a.i0 + a.n_gen);
-    const size_t off = (((size_t)c * a.Hkv + g) * (size_t)a.cap + r0) * W::ROW;
-    KeyList L;
-    list_init(L);
-    list_add(L, a.gk + off, a.gv + off, r1 - r0);
-    WaveState<D> S;
-    state_init(S);
-    wave_stream<D>(L, wave, kWaves, qb, a.qk_scale, buf + wave * W::LDS, S);
-    state_finish(S);
-    const __amdgpu_buffer_rsrc_t r = part_rsrc(a);
-    const uint32_t slot = slot_off(a, c, g, a.n_p + gk);
-    waves_merge<D, G>(S, buf, [&](int h, int d, float M, float L, f32x4_t O) {
-        part_store4(r, slot + (uint32_t)(h * D + d) * 4u, O);
-        if (d == 0) {
-            part_store1(r, slot + (uint32_t)(G * D + h) * 4u, M);
-            part_store1(r, slot + (uint32_t)(G * D + G + h) * 4u, L);
-        }
-    });
-}
-
 // Prompt chunk of one (cell, KV head) on the vector ALUs (f32 inputs): each
 // key is read from the clean or the donor cache by pointer; ZERO slots are
 // skipped (their closed-form term is added when the partials are merged).
@@ -379,233 +348,6 @@ __device__ void prompt_item_valu(const AttnArgs &a, int c, int g, int pk, char *
                             },
                             m, l, o);
     valu_store_partial<D, G, BF16>(a, m, l, o, buf, slot_off(a, c, g, pk));
-}
-
-// One thread's share of staging a KT-key prompt tile: K in 16-byte units
-// (row-major in LDS), V in units of 4 keys x 8 d (transposed in LDS, so the
-// p.v operand reads key-contiguous words).
-template <int D>
-struct TileIo {
-    static constexpr int KT = 64;
-    static constexpr int KROW = D * 2 + 16;
-    static constexpr int VROW = KT * 2 + 8;
-    static constexpr int KUNITS = KT * (D / 8);
-    static constexpr int VUNITS = (D / 8) * (KT / 4);
-    static constexpr int NKU = KUNITS / kThreads;
-    static constexpr int NVU = VUNITS >= kThreads ? VUNITS / kThreads : 1;
-};
-
-template <int D>
-__device__ __forceinline__ void tile_fetch(u32x4_t (&kreg)[TileIo<D>::NKU], u32x4_t (&vreg)[TileIo<D>::NVU][4],
-                                           const char *Kg, const char *Vg, int t0, int t1) {
-    using T = TileIo<D>;
-    const int tid = threadIdx.x;
-    static_for<0, T::NKU>([&](auto n) {
-        const int u = tid + n * kThreads;
-        const int r = u / (D / 8), part = u % (D / 8);
-        const int key = min(t0 + r, t1 - 1);
-        kreg[n] = *reinterpret_cast<const u32x4_t *>(Kg + (size_t)key * (D * 2) + part * 16);
-    });
-    static_for<0, T::NVU>([&](auto n) {
-        const int u = tid + n * kThreads;
-        const int dg = u % (D / 8), kq = (u / (D / 8)) % (T::KT / 4);   // in range for every lane
-        static_for<0, 4>([&](auto kk) {
-            const int key = min(t0 + 4 * kq + kk, t1 - 1);
-            vreg[n][kk] = *reinterpret_cast<const u32x4_t *>(Vg + (size_t)key * (D * 2) + dg * 16);
-        });
-    });
-}
-
-template <int D>
-__device__ __forceinline__ void tile_stage(const u32x4_t (&kreg)[TileIo<D>::NKU], const u32x4_t (&vreg)[TileIo<D>::NVU][4],
-                                           char *sK, char *sV) {
-    using T = TileIo<D>;
-    const int tid = threadIdx.x;
-    static_for<0, T::NKU>([&](auto n) {
-        const int u = tid + n * kThreads;
-        const int r = u / (D / 8), part = u % (D / 8);
-        *reinterpret_cast<u32x4_t *>(sK + r * T::KROW + part * 16) = kreg[n];
-    });
-    static_for<0, T::NVU>([&](auto n) {
-        const int u = tid + n * kThreads;
-        if (u < T::VUNITS) {
-            const int dg = u % (D / 8), kq = u / (D / 8);
-            static_for<0, 8>([&](auto j) {
-                constexpr int jj = decltype(j)::value;
-                constexpr uint32_t sel = (jj & 1) ? 0x07060302u : 0x05040100u;
-                const uint32_t lo = __builtin_amdgcn_perm(vreg[n][1][jj >> 1], vreg[n][0][jj >> 1], sel);
-                const uint32_t hi = __builtin_amdgcn_perm(vreg[n][3][jj >> 1], vreg[n][2][jj >> 1], sel);
-                *reinterpret_cast<u32x2_t *>(sV + (8 * dg + jj) * T::VROW + 8 * kq) = u32x2_t{lo, hi};
-            });
-        }
-    });
-}
-
-template <int D, int G>
-__device__ void prompt_item_mfma(const AttnArgs &a, int g, int rb, int pk, char *buf) {
-    using L = Lds<D, G, true>;
-    constexpr int KT = L::KT, KROW = L::KROW, VROW = L::VROW;
-    constexpr int NDS = D / 32;   // k-steps of q.k
-    constexpr int NDT = D / 16;   // 16-wide d tiles of the output
-    char *sK = buf;
-    char *sV = buf + KT * KROW;
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int col = lane & 15, quad = lane >> 4;
-
-    const int R = rb * kRowBlock + wave * 16 + col;
-    const int cidx = R / G;
-    const bool row_ok = cidx < a.C;
-    const int cell = row_ok ? a.order[cidx] : 0;
-    const int hl = R % G;
-    const bool spl = row_ok && bit_set(a.spliced, cell);
-    const bool row_clean = row_ok && !spl;
-    const bool row_donor = spl && !a.zero_donor;
-    const int first = rb * kRowBlock / G;
-    const int last = min(a.C, (rb + 1) * kRowBlock / G) - 1;
-    const bool blk_clean = first < a.n_clean;
-    const bool blk_donor = !a.zero_donor && last >= a.n_clean;
-
-    bf16x8_t qf[NDS];
-    {
-        const char *qrow = a.q + ((size_t)cell * a.Hq + (size_t)g * G + hl) * (D * 2);
-        static_for<0, NDS>([&](auto st) {
-            uint4 w = make_uint4(0, 0, 0, 0);
-            if (row_ok) w = *reinterpret_cast<const uint4 *>(qrow + (32 * st + 8 * quad) * 2);
-            qf[st] = __builtin_bit_cast(bf16x8_t, w);
-        });
-    }
-    f32x4_t o[NDT];
-    static_for<0, NDT>([&](auto t) { o[t] = f32x4_t{0.f, 0.f, 0.f, 0.f}; });
-    float m = -INFINITY, lsum = 0.f;
-
-    const int k0 = a.jp0 + pk * a.p_len;
-    const int k1 = min(k0 + a.p_len, a.Tp);
-    const size_t head = (size_t)g * a.Tp * (D * 2);
-
-    // The chunk is a sequence of steps (tile, source).  Tiles hold up to KT
-    // keys and never straddle a span boundary (a tile is all span or all
-    // not), so a row's keys are grouped the same whether it is spliced or
-    // not.  A tile runs a clean pass if any row reads it from the clean cache
-    // and a donor pass if any spliced row reads it from the donor cache.
-    auto tile_end = [&](int t0) __attribute__((always_inline)) {
-        int t1 = min(t0 + KT, k1);
-        if (t0 < a.sa) t1 = min(t1, a.sa);
-        else if (t0 < a.sb) t1 = min(t1, a.sb);
-        return t1;
-    };
-    auto needed = [&](int t0, int dpass) __attribute__((always_inline)) {
-        const bool span = t0 >= a.sa && t0 < a.sb;
-        return dpass ? (span && blk_donor) : (!span || blk_clean);
-    };
-    auto advance = [&](int &t0, int &dpass) __attribute__((always_inline)) {   // to the next needed step, t0 = k1 at the end
-        for (;;) {
-            if (dpass == 0) {
-                dpass = 1;
-            } else {
-                t0 = tile_end(t0);
-                dpass = 0;
-            }
-            if (t0 >= k1 || needed(t0, dpass)) return;
-        }
-    };
-
-    // this thread's share of a tile: K units (16 bytes) and V units (4 keys x 8 d)
-    u32x4_t kreg[TileIo<D>::NKU];
-    u32x4_t vreg[TileIo<D>::NVU][4];
-
-    int t0 = k0, dpass = 0;
-    if (t0 < k1 && !needed(t0, 0)) advance(t0, dpass);
-    if (t0 < k1)
-        tile_fetch<D>(kreg, vreg, pick_base(dpass, a.ck, a.dk) + head, pick_base(dpass, a.cv, a.dv) + head, t0,
-                      tile_end(t0));
-    while (t0 < k1) {
-        const int t1 = tile_end(t0);
-        const int cur_dpass = dpass;
-        __syncthreads();   // the previous step no longer reads the LDS tiles
-        tile_stage<D>(kreg, vreg, sK, sV);
-        __syncthreads();
-        int nt0 = t0, ndpass = dpass;
-        advance(nt0, ndpass);
-        if (nt0 < k1)   // in flight while this step computes
-            tile_fetch<D>(kreg, vreg, pick_base(ndpass, a.ck, a.dk) + head, pick_base(ndpass, a.cv, a.dv) + head, nt0,
-                          tile_end(nt0));
-
-        f32x4_t s[4];
-        static_for<0, 4>([&](auto sub) {
-            s[sub] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-            static_for<0, NDS>([&](auto st) {
-                const bf16x8_t kf = *reinterpret_cast<const bf16x8_t *>(
-                    sK + (16 * sub + col) * KROW + (32 * st + 8 * quad) * 2);
-                s[sub] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[st], s[sub], 0, 0, 0);
-            });
-        });
-        float p[4][4];
-        float mt = -INFINITY;
-#pragma unroll
-        for (int sub = 0; sub < 4; ++sub)
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                const int key = t0 + 16 * sub + 4 * quad + i;
-                const bool in_span = key >= a.sa && key < a.sb;
-                const bool ok = row_ok && key < t1 &&
-                                (cur_dpass ? (in_span && row_donor) : (!in_span || row_clean));
-                p[sub][i] = ok ? s[sub][i] * a.qk_scale : -INFINITY;
-                mt = fmaxf(mt, p[sub][i]);
-            }
-        mt = fmaxf(mt, __shfl_xor(mt, 16));
-        mt = fmaxf(mt, __shfl_xor(mt, 32));
-        const bool need = mt > m + kSlack;
-        if (__any(need)) {
-            // only rows that need it move their maximum: a row's arithmetic
-            // never depends on the other rows of its wave
-            const float mn = need ? fmaxf(m, mt) : m;
-            const float al = need ? fast_exp2(m - (mn == -INFINITY ? 0.f : mn)) : 1.f;
-            lsum *= al;
-            static_for<0, NDT>([&](auto t) { o[t] *= al; });
-            m = mn;
-        }
-        const float ms = m == -INFINITY ? 0.f : m;
-#pragma unroll
-        for (int sub = 0; sub < 4; ++sub)
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                p[sub][i] = fast_exp2(p[sub][i] - ms);
-                lsum += p[sub][i];
-            }
-        static_for<0, 2>([&](auto kg) {
-            bf16x8_t ph, pl;
-            static_for<0, 8>([&](auto j) {
-                constexpr int jj = decltype(j)::value;
-                const float x = p[2 * kg + (jj >> 2)][jj & 3];
-                const __bf16 hb = (__bf16)x;
-                ph[jj] = hb;
-                pl[jj] = (__bf16)(x - (float)hb);
-            });
-            static_for<0, NDT>([&](auto t) {
-                const char *vrow = sV + (16 * t + col) * VROW;
-                const uint2 va = *reinterpret_cast<const uint2 *>(vrow + (32 * kg + 4 * quad) * 2);
-                const uint2 vb = *reinterpret_cast<const uint2 *>(vrow + (32 * kg + 16 + 4 * quad) * 2);
-                const bf16x8_t vf = __builtin_bit_cast(bf16x8_t, make_uint4(va.x, va.y, vb.x, vb.y));
-                o[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, ph, o[t], 0, 0, 0);
-                o[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pl, o[t], 0, 0, 0);
-            });
-        });
-        t0 = nt0;
-        dpass = ndpass;
-    }
-    lsum += __shfl_xor(lsum, 16);
-    lsum += __shfl_xor(lsum, 32);
-    if (row_ok) {
-        const __amdgpu_buffer_rsrc_t r = part_rsrc(a);
-        const uint32_t slot = slot_off(a, cell, g, pk);
-        static_for<0, NDT>([&](auto t) {
-            part_store4(r, slot + (uint32_t)(hl * D + 16 * t + 4 * quad) * 4u, o[t]);
-        });
-        if (quad == 0) {
-            part_store1(r, slot + (uint32_t)(G * D + hl) * 4u, m);
-            part_store1(r, slot + (uint32_t)(G * D + G + hl) * 4u, lsum);
-        }
-    }
 }
 
 // ----------------------------------------------------------- merging
@@ -719,61 +461,188 @@ __device__ void combine_cells(const AttnArgs &a, const int *list, int n, int g, 
                            __HIP_MEMORY_SCOPE_AGENT);
 }
 
-// One launch per call: blocks [0, n_prompt_items) are prompt items, the
-// rest generated-row items.
-template <int D, int G, bool BF16>
-__global__ __launch_bounds__(kThreads) void attn_kernel(AttnArgs a) {
+// Waves per SIMD the register allocation must allow: the bf16 streams fit 4
+// (128 VGPRs) at D <= 128 and 2 at D = 256.
+constexpr int waves_per_simd(int D) { return D <= 128 ? 4 : 2; }
+
+// f32 inputs, one launch per call: blocks [0, n_prompt_items) are prompt
+// items (cell, KV head, prompt chunk), the rest generated-row items; the
+// last item of a (cell, KV head) merges its partials.
+template <int D, int G>
+__global__ __launch_bounds__(kThreads) void items_kernel(AttnArgs a) {
+    constexpr bool BF16 = false;
     __shared__ __attribute__((aligned(16))) char buf[Lds<D, G, BF16>::BYTES];
-    __shared__ int s_list[kRowBlock + 1];
+    __shared__ int s_list[2];
     const int tid = threadIdx.x;
     int item = blockIdx.x;
+    int c, g;
     if (item < a.n_prompt_items) {
         const int pk = item % a.n_p;
         item /= a.n_p;
-        if constexpr (BF16) {
-            const int rb = item % a.n_rb;
-            const int g = item / a.n_rb;
-            prompt_item_mfma<D, G>(a, g, rb, pk, buf);
-            if (tid == 0) s_list[0] = 0;
-            stores_performed();
-            const int first = rb * kRowBlock / G;
-            const int n_cells = min(a.C, first + kRowBlock / G) - first;
-            if (tid < n_cells) {
-                const int cell = a.order[first + tid];
-                if (arrive(a, cell, g)) s_list[1 + atomicAdd(&s_list[0], 1)] = cell;
-            }
-            __syncthreads();
-            if (s_list[0] > 0) combine_cells<D, G>(a, s_list + 1, s_list[0], g, buf);
-        } else {
-            const int g = item % a.Hkv;
-            const int c = item / a.Hkv;
-            prompt_item_valu<D, G, BF16>(a, c, g, pk, buf);
-            stores_performed();
-            if (tid == 0) {
-                s_list[0] = arrive(a, c, g) ? 1 : 0;
-                s_list[1] = c;
-            }
-            __syncthreads();
-            if (s_list[0]) combine_cells<D, G>(a, s_list + 1, 1, g, buf);
-        }
+        g = item % a.Hkv;
+        c = item / a.Hkv;
+        prompt_item_valu<D, G, BF16>(a, c, g, pk, buf);
     } else {
         item -= a.n_prompt_items;
         const int gk = item % a.n_g;
         item /= a.n_g;
-        const int g = item % a.Hkv;
-        const int c = item / a.Hkv;
-        if constexpr (BF16)
-            gen_item_mfma<D, G>(a, c, g, gk, buf);
-        else
-            gen_item<D, G, BF16>(a, c, g, gk, buf);
-        stores_performed();
-        if (tid == 0) {
-            s_list[0] = arrive(a, c, g) ? 1 : 0;
-            s_list[1] = c;
-        }
-        __syncthreads();
-        if (s_list[0]) combine_cells<D, G>(a, s_list + 1, 1, g, buf);
+        g = item % a.Hkv;
+        c = item / a.Hkv;
+        gen_item<D, G, BF16>(a, c, g, gk, buf);
     }
+    stores_performed();
+    if (tid == 0) {
+        s_list[0] = arrive(a, c, g) ? 1 : 0;
+        s_list[1] = c;
+    }
+    __syncthreads();
+    if (s_list[0]) combine_cells<D, G>(a, s_list + 1, 1, g, buf);
+}
+
+// ------------------------------------------------------- bf16, long prompts
+//
+// Launch 1: the shared-prompt contraction (prompt_wide.hpp).  Work group =
+// (KV head, group of Wide<D>::ROWS rows, prompt chunk); a group holds rows of
+// unspliced cells only or of spliced cells only.  Every row it owns gets one
+// partial result (o, m, l) for the chunk, stored with plain stores: launch 2
+// runs after this kernel has completed, which makes them visible.
+template <int D, int G>
+__global__ __launch_bounds__(kThreads) void prompt_wide_kernel(AttnArgs a) {
+    using X = Wide<D>;
+    __shared__ __attribute__((aligned(16))) char lds[X::LDS];
+    int item = blockIdx.x;
+    const int pk = item % a.n_p;
+    item /= a.n_p;
+    const int rg = item % a.n_rb;
+    const int g = item / a.n_rb;
+    const int lane = threadIdx.x & 63, col = lane & 15, quad = lane >> 4;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    ColMask cm[X::RB];
+    bf16x8_t qb[X::RB][X::NDS];
+    int cell[X::RB], hh[X::RB];
+    int clean_here = 0, donor_here = 0;
+    // row groups of unspliced cells come first; a group never mixes classes
+    const bool clean_group = rg < a.n_rg_clean;
+    const int first_cell = clean_group ? 0 : a.n_clean;
+    const int end_cell = clean_group ? a.n_clean : a.C;
+    const int grp = clean_group ? rg : rg - a.n_rg_clean;
+    static_for<0, X::RB>([&](auto rb) {
+        const int R = grp * X::ROWS + (wave * X::RB + rb) * 16 + col;
+        const int cidx = first_cell + R / G;
+        const bool ok = cidx < end_cell;
+        cell[rb] = ok ? a.order[cidx] : 0;
+        hh[rb] = R % G;
+        const bool spl = ok && bit_set(a.spliced, cell[rb]);
+        cm[rb] = ColMask{ok, ok && !spl, spl && !a.zero_donor};
+        clean_here |= cm[rb].clean ? 1 : 0;
+        donor_here |= cm[rb].donor ? 1 : 0;
+        load_q_cols<D>(ok ? a.q + ((size_t)cell[rb] * a.Hq + (size_t)g * G + hh[rb]) * X::ROW : nullptr, qb[rb]);
+    });
+    // the span passes the work group needs: clean rows read the clean span,
+    // spliced rows the donor span (a ZERO splice reads none)
+    const bool any_clean = __builtin_amdgcn_readfirstlane(__syncthreads_or(clean_here)) != 0;
+    const bool any_donor = __builtin_amdgcn_readfirstlane(__syncthreads_or(donor_here)) != 0;
+
+    const int k0 = a.jp0 + pk * a.p_len;
+    const int k1 = min(k0 + a.p_len, a.Tp);
+    const size_t head = (size_t)g * a.Tp * X::ROW;
+    const char *ck = a.ck + head, *cv = a.cv + head;
+    const int pre1 = min(k1, a.sa), sp0 = max(k0, a.sa), sp1 = min(k1, a.sb), post0 = max(k0, a.sb);
+    KeyList L;
+    list_init(L);
+    list_add<X::TK>(L, ck + (size_t)k0 * X::ROW, cv + (size_t)k0 * X::ROW, pre1 - k0);
+    if (any_clean)
+        list_add<X::TK>(L, ck + (size_t)sp0 * X::ROW, cv + (size_t)sp0 * X::ROW, sp1 - sp0, kColsClean);
+    if (any_donor) {
+        const char *dk = a.dk + head, *dv = a.dv + head;
+        list_add<X::TK>(L, dk + (size_t)sp0 * X::ROW, dv + (size_t)sp0 * X::ROW, sp1 - sp0, kColsDonor);
+    }
+    list_add<X::TK>(L, ck + (size_t)post0 * X::ROW, cv + (size_t)post0 * X::ROW, k1 - post0);
+
+    WideState<D> S;
+    static_for<0, X::RB>([&](auto rb) {
+        static_for<0, X::NDT>([&](auto t) { S.o[rb][t] = f32x4_t{0.f, 0.f, 0.f, 0.f}; });
+        S.m[rb] = -INFINITY;
+        S.lsum[rb] = 0.f;
+    });
+    wide_stream<D>(L, cm, qb, a.qk_scale, lds, S);
+
+    char *part = reinterpret_cast<char *>(a.part);
+    static_for<0, X::RB>([&](auto rb) {
+        float l = S.lsum[rb];
+        l += __shfl_xor(l, 16);
+        l += __shfl_xor(l, 32);
+        if (cm[rb].all) {
+            char *slot = part + slot_off(a, cell[rb], g, pk);
+            static_for<0, X::NDT>([&](auto t) {
+                *reinterpret_cast<f32x4_t *>(slot + (size_t)(hh[rb] * D + 16 * t + 4 * quad) * 4) = S.o[rb][t];
+            });
+            if (quad == 0) {
+                *reinterpret_cast<float *>(slot + (size_t)(G * D + hh[rb]) * 4) = S.m[rb];
+                *reinterpret_cast<float *>(slot + (size_t)(G * D + G + hh[rb]) * 4) = l;
+            }
+        }
+    });
+}
+
+// Launch 2: one work group per (cell, KV head) streams the cell's generated
+// rows (four waves, interleaved tiles, non-temporal loads), merges its waves,
+// folds in the prompt partials of launch 1 in chunk order and then the ZERO
+// term (n_zero keys of score 0 and value 0), and writes out and lse.
+template <int D, int G>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(waves_per_simd(D))))
+void gen_merge_kernel(AttnArgs a) {
+    using W = WaveMfma<D>;
+    __shared__ __attribute__((aligned(16))) char buf[CellwiseLds<D, G>::BYTES];
+    const int g = blockIdx.x % a.Hkv;
+    const int c = blockIdx.x / a.Hkv;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int col = threadIdx.x & 15;
+    bf16x8_t qb[W::NDS];
+    load_q_cols<D>(a.q + ((size_t)c * a.Hq + (size_t)g * G + col % G) * W::ROW, qb);
+    const size_t goff = (((size_t)c * a.Hkv + g) * (size_t)a.cap + a.i0) * W::ROW;
+    KeyList L;
+    list_init(L);
+    list_add(L, a.gk + goff, a.gv + goff, a.n_gen, kColsAll, true);
+    WaveState<D> S;
+    state_init(S);
+    const ColMask cm{true, true, true};
+    wave_stream<D>(L, wave, kWaves, cm, qb, a.qk_scale, buf + wave * W::LDS, S);
+    state_finish(S);
+
+    const bool zero_term = a.zero_donor && bit_set(a.spliced, c) && a.sb > a.sa;
+    const char *part = reinterpret_cast<const char *>(a.part);
+    const size_t base = slot_off(a, c, g, 0);
+    const size_t slot_bytes = (size_t)a.slot_floats * 4;
+    waves_merge<D, G>(S, buf, [&](int h, int d, float M, float Lsum, f32x4_t O) {
+        auto fold = [&](float mk, float lk, f32x4_t ok) __attribute__((always_inline)) {
+            const float mn = fmaxf(M, mk);
+            const float ms = mn == -INFINITY ? 0.f : mn;
+            const float fo = fast_exp2(M - ms), fn = fast_exp2(mk - ms);
+            Lsum = Lsum * fo + lk * fn;
+            O = O * fo + ok * fn;
+            M = mn;
+        };
+        constexpr int B = 8;
+        for (int k0 = 0; k0 < a.n_slots; k0 += B) {
+            f32x4_t ok[B];
+            float mk[B], lk[B];
+#pragma unroll
+            for (int j = 0; j < B; ++j) {
+                const char *sb = part + base + (size_t)min(k0 + j, a.n_slots - 1) * slot_bytes;
+                ok[j] = *reinterpret_cast<const f32x4_t *>(sb + (size_t)(h * D + d) * 4);
+                mk[j] = *reinterpret_cast<const float *>(sb + (size_t)(G * D + h) * 4);
+                lk[j] = *reinterpret_cast<const float *>(sb + (size_t)(G * D + G + h) * 4);
+            }
+#pragma unroll
+            for (int j = 0; j < B; ++j)
+                if (k0 + j < a.n_slots) fold(mk[j], lk[j], ok[j]);
+        }
+        if (zero_term) fold(0.f, (float)(a.sb - a.sa), f32x4_t{0.f, 0.f, 0.f, 0.f});
+        const int row = c * a.Hq + g * G + h;
+        *reinterpret_cast<f32x4_t *>(a.out + (size_t)row * D + d) = O * (1.f / Lsum);
+        if (d == 0) a.lse[row] = (M + log2f(Lsum)) * kLn2;
+    });
 }
 
 // ------------------------------------------------------- cellwise kernel
@@ -840,14 +709,16 @@ __global__ __launch_bounds__(kThreads) void cellwise_kernel(AttnArgs a) {
 // and the span segment exists whether or not the cell is spliced, so a
 // splice never moves a tile boundary.
 template <int D, int G>
-__global__ __launch_bounds__(kThreads) void cellwise_mfma_kernel(AttnArgs a) {
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(waves_per_simd(D))))
+void cellwise_mfma_kernel(AttnArgs a) {
     using W = WaveMfma<D>;
     __shared__ __attribute__((aligned(16))) char buf[CellwiseLds<D, G>::BYTES];
     const int g = blockIdx.x % a.Hkv;
     const int c = blockIdx.x / a.Hkv;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);   // uniform: tile pointers stay scalar
+    const int col = threadIdx.x & 15;
     bf16x8_t qb[W::NDS];
-    load_q_mfma<D, G>(a.q + ((size_t)c * a.Hq + (size_t)g * G) * W::ROW, qb);
+    load_q_cols<D>(a.q + ((size_t)c * a.Hq + (size_t)g * G + col % G) * W::ROW, qb);
     const bool spl = bit_set(a.spliced, c);
     const bool zskip = spl && a.zero_donor;
     const bool from_donor = spl && !a.zero_donor;
@@ -862,10 +733,11 @@ __global__ __launch_bounds__(kThreads) void cellwise_mfma_kernel(AttnArgs a) {
         list_add(L, a.ck + head + (size_t)a.sb * W::ROW, a.cv + head + (size_t)a.sb * W::ROW, a.Tp - a.sb);
     }
     const size_t goff = (((size_t)c * a.Hkv + g) * (size_t)a.cap + a.i0) * W::ROW;
-    list_add(L, a.gk + goff, a.gv + goff, a.n_gen);
+    list_add(L, a.gk + goff, a.gv + goff, a.n_gen, kColsAll, true);
     WaveState<D> S;
     state_init(S);
-    wave_stream<D>(L, wave, kWaves, qb, a.qk_scale, buf + wave * W::LDS, S);
+    const ColMask cm{true, true, true};
+    wave_stream<D>(L, wave, kWaves, cm, qb, a.qk_scale, buf + wave * W::LDS, S);
     state_finish(S);
     const int nsv = a.sb - a.sa;
     const bool zero_term = zskip && nsv > 0;
@@ -887,15 +759,18 @@ __global__ __launch_bounds__(kThreads) void cellwise_mfma_kernel(AttnArgs a) {
 
 typedef void (*attn_fn)(AttnArgs);
 struct AttnKernels {
-    attn_fn rowblock, cellwise;
+    attn_fn items;      // f32: one launch of prompt and generated items
+    attn_fn cellwise;   // short prompts: one work group per (cell, KV head)
+    attn_fn prompt;     // bf16 launch 1: shared-prompt contraction
+    attn_fn gen;        // bf16 launch 2: generated rows and the merge
 };
 
 template <int D, int G, bool BF16>
 AttnKernels kernels_of() {
     if constexpr (BF16)
-        return AttnKernels{attn_kernel<D, G, BF16>, cellwise_mfma_kernel<D, G>};
+        return AttnKernels{nullptr, cellwise_mfma_kernel<D, G>, prompt_wide_kernel<D, G>, gen_merge_kernel<D, G>};
     else
-        return AttnKernels{attn_kernel<D, G, BF16>, cellwise_kernel<D, G, BF16>};
+        return AttnKernels{items_kernel<D, G>, cellwise_kernel<D, G, BF16>, nullptr, nullptr};
 }
 
 template <int D, bool BF16>
@@ -905,7 +780,7 @@ AttnKernels pick_g(int G) {
     case 2: return kernels_of<D, 2, BF16>();
     case 4: return kernels_of<D, 4, BF16>();
     case 8: return kernels_of<D, 8, BF16>();
-    default: return AttnKernels{nullptr, nullptr};
+    default: return AttnKernels{nullptr, nullptr, nullptr, nullptr};
     }
 }
 

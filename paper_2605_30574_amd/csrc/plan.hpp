@@ -99,21 +99,33 @@ inline bool cell_spliced(const int32_t *cell_LW, int c, int layer, int step) {
 
 // ---------------------------------------------------------------- attention plan
 //
-// One call = one launch of prompt work items and generated-span work items.
-//   prompt items (bf16): (KV head, block of kRowBlock rows, prompt chunk); the
-//     rows of a KV head are the (cell, q head) pairs of every cell, clean
-//     cells first, so one staged K/V tile serves kRowBlock rows;
-//   prompt items (f32):  (cell, KV head, prompt chunk), on the vector ALUs;
-//   generated items:     (cell, KV head, chunk of the generated rows).
-// Every (cell, KV head) receives one partial result per prompt chunk and per
-// generated chunk; the last of them to finish merges them.
+// bf16 inputs:
+//   cellwise (prompt of at most kCellwiseMaxPrompt visible keys): one launch,
+//     one work group per (cell, KV head) streaming the cell's whole list;
+//   otherwise two launches:
+//     1. prompt kernel: work groups (KV head, group of wide_rows(D) rows,
+//        prompt chunk); the rows of a KV head are the (cell, q head) pairs of
+//        every cell, clean cells first, and each K/V tile is staged in LDS
+//        once for all of them; every row gets one partial result per chunk;
+//     2. generated-row kernel: one work group per (cell, KV head) streams the
+//        cell's generated rows and folds in its prompt partials.
+// f32 inputs (vector ALUs, one launch): prompt items (cell, KV head, prompt
+//   chunk) and generated items (cell, KV head, generated chunk); the last item
+//   of a (cell, KV head) to finish merges its partials.
 
-constexpr int kRowBlock = 64;              // rows per bf16 prompt item
+constexpr int kRowBlock = 64;              // rows of the f32 merge staging
 constexpr int kMinChunk = 256;             // a default chunk is at least this long
 constexpr int kMaxChunks = 32;             // default chunks per part (prompt, generated)
 constexpr int kMaxSlots = 64;              // partial results per (cell, KV head)
-constexpr int kPromptItemsTarget = 512;    // prompt items a default split aims for
-constexpr int kGenItemsTarget = 2048;      // generated items a default split aims for
+constexpr int kPromptItemsTarget = 512;    // f32 prompt items a default split aims for
+constexpr int kGenItemsTarget = 2048;      // f32 generated items a default split aims for
+constexpr int kWideItemsTarget = 512;      // bf16 prompt work groups a default split aims for
+
+// bf16 prompt kernel: 16-row MFMA blocks per wave (so that a wave's output
+// accumulators, RB * D / 4 registers, stay at 64) and rows per work group
+// (four waves).
+constexpr int wide_row_blocks(int D) { return 256 / D; }
+constexpr int wide_rows(int D) { return 4 * 16 * wide_row_blocks(D); }
 
 inline int ceil_div(int64_t a, int64_t b) { return (int)((a + b - 1) / b); }
 inline int round_up(int64_t a, int64_t m) { return (int)((a + m - 1) / m * m); }
@@ -121,24 +133,40 @@ inline int round_up(int64_t a, int64_t m) { return (int)((a + m - 1) / m * m); }
 // Floats per partial-result slot: o[G][D], m[G], l[G], padded to 256 bytes.
 inline int slot_floats(int G, int D) { return (G * D + 2 * G + 63) / 64 * 64; }
 
-inline bool mfma_prompt(const splice_shape &sh) { return sh.dtype == SPLICE_BF16; }
+inline bool bf16_path(const splice_shape &sh) { return sh.dtype == SPLICE_BF16; }
 
-inline int row_blocks(const splice_shape &sh) {
-    return ceil_div((int64_t)sh.n_cells * group_of(sh), kRowBlock);
+// bf16 row groups of one KV head: the rows of unspliced cells and the rows
+// of spliced cells are grouped separately (wide_rows(D) rows per group), so
+// no group needs both the clean and the donor span.  n_clean cells of C are
+// unspliced at the call.
+inline int clean_row_groups(const splice_shape &sh, int n_clean) {
+    return ceil_div((int64_t)n_clean * group_of(sh), wide_rows(sh.head_dim));
+}
+inline int row_groups(const splice_shape &sh, int n_clean) {
+    return clean_row_groups(sh, n_clean) +
+           ceil_div((int64_t)(sh.n_cells - n_clean) * group_of(sh), wide_rows(sh.head_dim));
 }
 
-// Prompt items per prompt chunk.
-inline int prompt_items_per_chunk(const splice_shape &sh) {
-    return sh.n_kv_heads * (mfma_prompt(sh) ? row_blocks(sh) : sh.n_cells);
+// Prompt work groups per prompt chunk.  The bf16 count depends on the call's
+// split of cells; the default chunking uses the split-independent bound
+// (one more row group than an unsplit grid).
+inline int prompt_items_per_chunk(const splice_shape &sh, int n_clean) {
+    return sh.n_kv_heads * (bf16_path(sh) ? row_groups(sh, n_clean) : sh.n_cells);
+}
+inline int prompt_items_bound(const splice_shape &sh) {
+    if (!bf16_path(sh)) return sh.n_kv_heads * sh.n_cells;
+    return sh.n_kv_heads * (ceil_div((int64_t)sh.n_cells * group_of(sh), wide_rows(sh.head_dim)) + 1);
 }
 
 inline int prompt_chunk_target(const splice_shape &sh) {
-    const int per = prompt_items_per_chunk(sh);
-    const int t = per > 0 ? kPromptItemsTarget / per : 1;
+    const int per = prompt_items_bound(sh);
+    const int want = bf16_path(sh) ? kWideItemsTarget : kPromptItemsTarget;
+    const int t = per > 0 ? want / per : 1;
     return t < 1 ? 1 : (t > kMaxChunks ? kMaxChunks : t);
 }
 
 inline int gen_chunk_target(const splice_shape &sh) {
+    if (bf16_path(sh)) return 1;   // one generated-row work group per (cell, KV head)
     const int64_t pairs = (int64_t)sh.n_cells * sh.n_kv_heads;
     const int64_t t = pairs > 0 ? kGenItemsTarget / pairs : 1;
     return t < 1 ? 1 : (t > kMaxChunks ? kMaxChunks : (int)t);
@@ -169,15 +197,22 @@ inline void cut(int n, int target, int split, int *k, int *len) {
 constexpr int kCellwiseMaxPrompt = 512;
 
 struct AttnPlan {
-    bool cellwise;           // one work group per (cell, KV head), no merge
+    bool cellwise;           // one work group per (cell, KV head), no partials
     Geometry geo;
     int n_p, p_len;          // prompt chunks over the visible prompt
     int n_g, g_len;          // chunks over the visible generated rows
-    int n_slots;             // n_p + n_g partial results per (cell, KV head)
+    int n_slots;             // partial results per (cell, KV head)
     int n_prompt_items, n_gen_items;
 };
 
-inline AttnPlan plan_attn(const splice_shape &sh, const splice_call &call) {
+// Cells of the call that are not spliced.
+inline int count_clean(const splice_shape &sh, const splice_call &call, const int32_t *cell_LW) {
+    int n = 0;
+    for (int c = 0; c < sh.n_cells; ++c) n += cell_spliced(cell_LW, c, call.layer, call.step) ? 0 : 1;
+    return n;
+}
+
+inline AttnPlan plan_attn(const splice_shape &sh, const splice_call &call, int n_clean) {
     AttnPlan p;
     p.geo = geometry(sh, call);
     p.cellwise = call.split_keys == 0 && p.geo.n_prompt <= kCellwiseMaxPrompt;
@@ -189,9 +224,16 @@ inline AttnPlan plan_attn(const splice_shape &sh, const splice_call &call) {
         return p;
     }
     cut(p.geo.n_prompt, prompt_chunk_target(sh), call.split_keys, &p.n_p, &p.p_len);
-    cut(p.geo.n_gen, gen_chunk_target(sh), call.split_keys, &p.n_g, &p.g_len);
-    p.n_slots = p.n_p + p.n_g;
-    p.n_prompt_items = prompt_items_per_chunk(sh) * p.n_p;
+    if (bf16_path(sh)) {
+        // the generated-row work group folds the prompt partials in itself
+        p.n_g = 1;
+        p.g_len = p.geo.n_gen;
+        p.n_slots = p.n_p;
+    } else {
+        cut(p.geo.n_gen, gen_chunk_target(sh), call.split_keys, &p.n_g, &p.g_len);
+        p.n_slots = p.n_p + p.n_g;
+    }
+    p.n_prompt_items = prompt_items_per_chunk(sh, n_clean) * p.n_p;
     p.n_gen_items = sh.n_cells * sh.n_kv_heads * p.n_g;
     return p;
 }
@@ -226,8 +268,8 @@ inline int max_default_chunks(int n, int target) {
 }
 
 inline int worst_default_slots(const splice_shape &sh) {
-    return max_default_chunks(sh.prompt_len, prompt_chunk_target(sh)) +
-           max_default_chunks(sh.gen_capacity, gen_chunk_target(sh));
+    const int prompt = max_default_chunks(sh.prompt_len, prompt_chunk_target(sh));
+    return bf16_path(sh) ? prompt : prompt + max_default_chunks(sh.gen_capacity, gen_chunk_target(sh));
 }
 
 }  // namespace splice

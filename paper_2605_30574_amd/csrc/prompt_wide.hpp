@@ -1,0 +1,214 @@
+// prompt_wide.hpp -- the shared-prompt contraction: many (cell, q head) rows
+// of one KV head against the same prompt tiles, on the matrix cores.
+//
+// A work group of four waves owns wide_rows(D) rows; each wave owns RB blocks
+// of 16 rows.  A 32-key tile of the prompt (K row-major, V transposed) is
+// staged in LDS once per work group and then, per wave,
+//   S  = K Q^T  : the K operand (16 keys x 32 d) is read from LDS once and
+//                 multiplied into all RB row blocks (v_mfma_f32_16x16x32_bf16);
+//   online softmax per row (column of S), masked per segment class;
+//   O^T += V^T P: each 16 d x 32 keys V^T operand is read once and multiplied
+//                 into all RB row blocks, P split into bf16 high and remainder.
+// The LDS tiles are double-buffered and the global loads of the next
+// DEPTH - 1 tiles are in flight while one is computed; one barrier per tile
+// orders the buffers.
+#pragma once
+
+#include "plan.hpp"
+#include "wave_mfma.hpp"
+
+namespace splice_dev {
+
+template <int D>
+struct Wide {
+    static constexpr int RB = splice::wide_row_blocks(D);   // 16-row blocks per wave
+    static constexpr int ROWS = splice::wide_rows(D);       // rows per work group
+    static constexpr int TK = 32;                           // keys per tile
+    static constexpr int ROW = D * 2;                       // bytes per K or V row
+    static constexpr int NDS = D / 32;                      // k-steps of q.k
+    static constexpr int NDT = D / 16;                      // 16-row d tiles of the output
+    static constexpr int KROW = ROW + 16;                   // K tile row stride in LDS (padded)
+    static constexpr int VROW = TK * 2 + 8;                 // V^T tile row stride in LDS (padded)
+    static constexpr int KTILE = TK * KROW;
+    static constexpr int BUF = KTILE + D * VROW;            // one staged tile
+    static constexpr int LDS = 2 * BUF;                     // double buffer
+    static constexpr int NKU = TK * (D / 8) / kThreads;     // 16-byte K units per thread
+    static constexpr int VU = (D / 8) * (TK / 4);           // V units (4 keys x 8 d): thread tid < VU owns one
+    static_assert(NKU >= 1 && VU <= kThreads, "tile staging assumes 64 <= D <= 256");
+};
+
+// One thread's share of a tile in flight.
+template <int D>
+struct WideRegs {
+    u32x4_t k[Wide<D>::NKU];
+    u32x4_t v[4];
+};
+
+template <int D>
+__device__ __forceinline__ void wide_fetch(const TileRef &t, WideRegs<D> &r) {
+    using X = Wide<D>;
+    const int tid = threadIdx.x;
+    const __amdgpu_buffer_rsrc_t rk = rows_rsrc(t.k, t.n * X::ROW);
+    const __amdgpu_buffer_rsrc_t rv = rows_rsrc(t.v, t.n * X::ROW);
+    static_for<0, X::NKU>([&](auto i) {
+        const int u = tid + kThreads * i;
+        r.k[i] = row_load<0>(rk, (u / (D / 8)) * X::ROW + (u % (D / 8)) * 16);
+    });
+    if (tid < X::VU) {
+        const int kq = tid & 7, dg = tid >> 3;   // keys 4 kq .. 4 kq + 3, bytes 16 dg ..
+        static_for<0, 4>([&](auto kk) { r.v[kk] = row_load<0>(rv, (4 * kq + kk) * X::ROW + 16 * dg); });
+    }
+}
+
+// K row-major (16-byte units), V transposed: row d holds the tile's keys.
+// Eight lanes of consecutive kq fill one 64-byte V^T row segment.
+template <int D>
+__device__ __forceinline__ void wide_stage(const WideRegs<D> &r, char *buf) {
+    using X = Wide<D>;
+    const int tid = threadIdx.x;
+    char *sK = buf;
+    char *sV = buf + X::KTILE;
+    static_for<0, X::NKU>([&](auto i) {
+        const int u = tid + kThreads * i;
+        *reinterpret_cast<u32x4_t *>(sK + (u / (D / 8)) * X::KROW + (u % (D / 8)) * 16) = r.k[i];
+    });
+    if (tid < X::VU) {
+        const int kq = tid & 7, dg = tid >> 3;
+        static_for<0, 8>([&](auto j) {
+            constexpr int jj = decltype(j)::value;
+            constexpr uint32_t sel = (jj & 1) ? 0x07060302u : 0x05040100u;
+            const uint32_t lo = __builtin_amdgcn_perm(r.v[1][jj >> 1], r.v[0][jj >> 1], sel);
+            const uint32_t hi = __builtin_amdgcn_perm(r.v[3][jj >> 1], r.v[2][jj >> 1], sel);
+            *reinterpret_cast<u32x2_t *>(sV + (8 * dg + jj) * X::VROW + 8 * kq) = u32x2_t{lo, hi};
+        });
+    }
+}
+
+// Streaming state of one wave: RB row blocks, lane (quad, col) holding row
+// block rb's column col (o[rb][t][i] = O^T[16 t + 4 quad + i][col]).
+template <int D>
+struct WideState {
+    f32x4_t o[Wide<D>::RB][Wide<D>::NDT];
+    float m[Wide<D>::RB];
+    float lsum[Wide<D>::RB];
+};
+
+// One staged tile for this wave's RB row blocks.  on[rb]: the tile's
+// segment is visible to this lane's row of block rb.
+template <int D>
+__device__ __forceinline__ void wide_compute(const char *buf, int n_valid, const bool (&on)[Wide<D>::RB],
+                                             const bf16x8_t (&qb)[Wide<D>::RB][Wide<D>::NDS], float qk_scale,
+                                             WideState<D> &S) {
+    using X = Wide<D>;
+    const int lane = threadIdx.x & 63, col = lane & 15, quad = lane >> 4;
+    const char *sK = buf;
+    const char *sV = buf + X::KTILE;
+    f32x4_t s[X::RB][2];
+    static_for<0, X::RB>([&](auto rb) {
+        s[rb][0] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+        s[rb][1] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    });
+    static_for<0, 2>([&](auto h) {
+        static_for<0, X::NDS>([&](auto st) {
+            const bf16x8_t kf = *reinterpret_cast<const bf16x8_t *>(
+                sK + (16 * h + col) * X::KROW + (32 * st + 8 * quad) * 2);
+            static_for<0, X::RB>([&](auto rb) {
+                s[rb][h] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qb[rb][st], s[rb][h], 0, 0, 0);
+            });
+        });
+    });
+    bf16x8_t ph[X::RB], pl[X::RB];
+    static_for<0, X::RB>([&](auto rb) {
+        float x[2][4];
+        float mt = -INFINITY;
+        static_for<0, 2>([&](auto h) {
+            static_for<0, 4>([&](auto i) {
+                const int key = 16 * h + 4 * quad + i;
+                x[h][i] = (on[rb] && key < n_valid) ? s[rb][h][(int)i] * qk_scale : -INFINITY;
+                mt = fmaxf(mt, x[h][i]);
+            });
+        });
+        mt = fmaxf(mt, __shfl_xor(mt, 16));
+        mt = fmaxf(mt, __shfl_xor(mt, 32));
+        const bool need = mt > S.m[rb] + kSlack;
+        if (__any(need)) {
+            const float mn = need ? fmaxf(S.m[rb], mt) : S.m[rb];
+            const float al = need ? fast_exp2(S.m[rb] - (mn == -INFINITY ? 0.f : mn)) : 1.f;
+            S.lsum[rb] *= al;
+            static_for<0, X::NDT>([&](auto t) { S.o[rb][t] *= al; });
+            S.m[rb] = mn;
+        }
+        const float ms = S.m[rb] == -INFINITY ? 0.f : S.m[rb];
+        static_for<0, 8>([&](auto j) {
+            constexpr int jj = decltype(j)::value;
+            const float p = fast_exp2(x[jj >> 2][jj & 3] - ms);
+            S.lsum[rb] += p;
+            const __bf16 hb = (__bf16)p;
+            ph[rb][jj] = hb;
+            pl[rb][jj] = (__bf16)(p - (float)hb);
+        });
+    });
+    // k-slot 8 quad + j is key 4 quad + j (j < 4) or 16 + 4 quad + (j - 4):
+    // the keys whose scores this lane holds
+    static_for<0, X::NDT>([&](auto t) {
+        const char *vrow = sV + (16 * t + col) * X::VROW;
+        const uint2 va = *reinterpret_cast<const uint2 *>(vrow + 8 * quad);
+        const uint2 vb = *reinterpret_cast<const uint2 *>(vrow + 32 + 8 * quad);
+        const bf16x8_t vf = __builtin_bit_cast(bf16x8_t, make_uint4(va.x, va.y, vb.x, vb.y));
+        static_for<0, X::RB>([&](auto rb) {
+            S.o[rb][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, ph[rb], S.o[rb][t], 0, 0, 0);
+            S.o[rb][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pl[rb], S.o[rb][t], 0, 0, 0);
+        });
+    });
+}
+
+// Tiles a work group keeps in flight: fetched into registers DEPTH - 1 tiles
+// ahead of the one being computed (the LDS tiles are double-buffered).
+template <int D>
+constexpr int wide_depth() { return D <= 128 ? 3 : 2; }
+
+// Stream every tile of the work group's list.  Iteration t computes the LDS
+// buffer t & 1, stages tile t + 1 from registers into the other buffer and
+// refills the freed registers with tile t + DEPTH; one barrier per tile
+// orders the buffers.  The loop is unrolled DEPTH times so that the register
+// sets are only ever indexed by constants.  Called by all threads of the
+// work group.
+template <int D>
+__device__ __forceinline__ void wide_stream(const KeyList &L, const ColMask (&cm)[Wide<D>::RB],
+                                            const bf16x8_t (&qb)[Wide<D>::RB][Wide<D>::NDS], float qk_scale,
+                                            char *lds, WideState<D> &S) {
+    using X = Wide<D>;
+    constexpr int DEPTH = wide_depth<D>();
+    const int n_tiles = list_tiles(L);
+    if (n_tiles == 0) return;
+    WideRegs<D> r[DEPTH];
+    TileRef ref[DEPTH];
+    static_for<0, DEPTH>([&](auto i) {
+        if (i < n_tiles) {
+            ref[i] = list_tile<X::TK>(L, i, X::ROW);
+            wide_fetch<D>(ref[i], r[i]);
+        }
+    });
+    wide_stage<D>(r[0], lds);
+    __syncthreads();
+    for (int base = 0; base < n_tiles; base += DEPTH) {
+        static_for<0, DEPTH>([&](auto j) {
+            constexpr int jn = (decltype(j)::value + 1) % DEPTH;
+            const int t = base + j;
+            if (t < n_tiles) {
+                const TileRef cur = ref[j];
+                if (t + DEPTH < n_tiles) {   // registers of tile t are free: refill them
+                    ref[j] = list_tile<X::TK>(L, t + DEPTH, X::ROW);
+                    wide_fetch<D>(ref[j], r[j]);
+                }
+                bool on[X::RB];
+                static_for<0, X::RB>([&](auto rb) { on[rb] = cm[rb].on(cur.cols); });
+                wide_compute<D>(lds + (t & 1) * X::BUF, cur.n, on, qb, qk_scale, S);
+                if (t + 1 < n_tiles) wide_stage<D>(r[jn], lds + ((t + 1) & 1) * X::BUF);
+                __syncthreads();   // the next buffer is staged; nobody reads this one any more
+            }
+        });
+    }
+}
+
+}  // namespace splice_dev

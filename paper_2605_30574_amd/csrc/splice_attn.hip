@@ -114,7 +114,7 @@ AttnKernels pick_attn(int D, int G, int dtype) {
     case 64: return bf16 ? attn_kernels_d64_bf16(G) : attn_kernels_d64_f32(G);
     case 128: return bf16 ? attn_kernels_d128_bf16(G) : attn_kernels_d128_f32(G);
     case 256: return bf16 ? attn_kernels_d256_bf16(G) : attn_kernels_d256_f32(G);
-    default: return AttnKernels{nullptr, nullptr};
+    default: return AttnKernels{nullptr, nullptr, nullptr, nullptr};
     }
 }
 
@@ -206,7 +206,7 @@ int64_t splice_decode_attn_workspace_bytes(const splice_shape *shape, const spli
     if (call) {
         rc = splice::validate_call(*shape, call);
         if (rc != SPLICE_OK) return rc;
-        n_slots = splice::plan_attn(*shape, *call).n_slots;
+        n_slots = splice::plan_attn(*shape, *call, 0).n_slots;   // slots do not depend on the cell split
         if (n_slots > splice::kMaxSlots) return SPLICE_EUNSUPPORTED;
     } else {
         n_slots = splice::worst_default_slots(*shape);
@@ -249,7 +249,8 @@ int32_t splice_decode_attn(const splice_shape *shape, const splice_call *call, c
     if (!zero && (!splice::aligned(donor_k, 16) || !splice::aligned(donor_v, 16))) return SPLICE_EINVAL;
     if (!splice::aligned(out, 16) || !splice::aligned(lse, 4)) return SPLICE_EINVAL;
 
-    const splice::AttnPlan plan = splice::plan_attn(sh, *call);
+    const int n_clean = splice::count_clean(sh, *call, cell_LW);
+    const splice::AttnPlan plan = splice::plan_attn(sh, *call, n_clean);
     if (plan.n_slots > splice::kMaxSlots) return SPLICE_EUNSUPPORTED;
     const splice::WorkspaceLayout wl = splice::workspace_layout(sh, plan.n_slots);
     if (!workspace || !splice::aligned(workspace, 256)) return SPLICE_EWORKSPACE;
@@ -257,7 +258,7 @@ int32_t splice_decode_attn(const splice_shape *shape, const splice_call *call, c
 
     const int G = splice::group_of(sh);
     const AttnKernels kern = pick_attn(sh.head_dim, G, sh.dtype);
-    if (!kern.rowblock) return SPLICE_EUNSUPPORTED;
+    if (!kern.cellwise) return SPLICE_EUNSUPPORTED;
 
     const splice::Geometry &geo = plan.geo;
     AttnArgs a;
@@ -277,7 +278,8 @@ int32_t splice_decode_attn(const splice_shape *shape, const splice_call *call, c
     a.n_p = plan.n_p; a.p_len = plan.p_len; a.n_g = plan.n_g; a.g_len = plan.g_len;
     a.n_slots = plan.n_slots;
     a.slot_floats = splice::slot_floats(G, sh.head_dim);
-    a.n_rb = splice::row_blocks(sh);
+    a.n_rb = splice::bf16_path(sh) ? splice::row_groups(sh, n_clean) : 0;
+    a.n_rg_clean = splice::bf16_path(sh) ? splice::clean_row_groups(sh, n_clean) : 0;
     a.n_prompt_items = plan.n_prompt_items;
     a.qk_scale = call->scale * kLog2e;
     fill_mask(sh, *call, cell_LW, a.spliced);
@@ -295,9 +297,22 @@ int32_t splice_decode_attn(const splice_shape *shape, const splice_call *call, c
                            (hipStream_t)stream, a);
         return launch_status();
     }
+    if (sh.dtype == SPLICE_BF16) {
+        // launch 1 writes the prompt partials, launch 2 streams the generated
+        // rows and merges; stream order makes launch 1's stores visible
+        if (plan.n_prompt_items > 0) {
+            hipLaunchKernelGGL(kern.prompt, dim3((unsigned)plan.n_prompt_items), dim3(kThreads), 0,
+                               (hipStream_t)stream, a);
+            const int32_t st = launch_status();
+            if (st != SPLICE_OK) return st;
+        }
+        hipLaunchKernelGGL(kern.gen, dim3((unsigned)(sh.n_cells * sh.n_kv_heads)), dim3(kThreads), 0,
+                           (hipStream_t)stream, a);
+        return launch_status();
+    }
     const int64_t items = (int64_t)plan.n_prompt_items + plan.n_gen_items;
     if (items > INT32_MAX) return SPLICE_EUNSUPPORTED;
-    hipLaunchKernelGGL(kern.rowblock, dim3((unsigned)items), dim3(kThreads), 0, (hipStream_t)stream, a);
+    hipLaunchKernelGGL(kern.items, dim3((unsigned)items), dim3(kThreads), 0, (hipStream_t)stream, a);
     return launch_status();
 }
 

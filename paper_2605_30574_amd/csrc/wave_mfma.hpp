@@ -1,27 +1,37 @@
-// wave_mfma.hpp -- one wave streams the K/V rows of one (cell, KV head)
-// through the matrix cores (bf16 inputs, fp32 accumulation).
+// wave_mfma.hpp -- one wave streams K/V rows through the matrix cores for 16
+// query rows at once (bf16 inputs, fp32 accumulation).
 //
-// The keys of a list are processed in tiles of 32.  For a tile the wave
-// computes, for all G query heads of the KV head at once,
+// The keys of a list are processed in tiles of 16.  For a tile the wave
+// computes, for its 16 query rows ("columns"),
 //   S = K Q^T   with v_mfma_f32_16x16x32_bf16: A = 16 keys x 32 d of K, loaded
-//               from memory straight into the operand layout; B = Q^T with
-//               the 16 columns holding heads (column j -> head j mod G);
+//               from memory straight into the operand layout; B = Q^T;
 //   online softmax per column (running maximum shared by the column's lanes);
-//   O^T += V^T P with the same instruction: A = 16 d x 32 keys of V^T, read
-//               from a per-wave LDS tile that holds V transposed; B = P, which
-//               stays in the lanes where S came out (split into a bf16 high
-//               part and a bf16 remainder, so p is carried to ~2^-17).
-// Waves never synchronise with each other while streaming: each owns its
-// LDS tile, and the next tile's loads are in flight while the current one is
-// computed.
+//   O^T += V^T P with v_mfma_f32_16x16x16_bf16: A = 16 d x 16 keys of V^T,
+//               read from a per-wave LDS tile that holds V transposed; B = P,
+//               which stays in the lanes where S came out, split into a bf16
+//               high part and a bf16 remainder (p carried to ~2^-17).
+// The 16 columns are either the G heads of one (cell, KV head) repeated
+// (column j -> head j mod G), or 16 different (cell, head) rows of one KV
+// head reading a shared prompt.  Waves never synchronise with each other
+// while streaming: each owns its LDS tile, and the next tile's loads are in
+// flight while the current one is computed.
 #pragma once
 
 #include "device_common.hpp"
 
 namespace splice_dev {
 
-constexpr int kTileKeys = 32;
+constexpr int kTileKeys = 16;
 constexpr int kMaxSeg = 4;
+
+typedef short i16x4_t __attribute__((ext_vector_type(4)));
+
+// Which columns a segment's keys are visible to.
+enum SegCols : int {
+    kColsAll = 0,     // every valid column
+    kColsClean = 1,   // columns of unspliced cells (span read from the clean cache)
+    kColsDonor = 2,   // columns of spliced cells (span read from the donor cache)
+};
 
 // An ordered key list made of up to kMaxSeg segments; the rows of a segment
 // are contiguous (row stride D bf16) from k[s] / v[s].  Tiles never straddle
@@ -30,6 +40,8 @@ struct KeyList {
     const char *k[kMaxSeg];
     const char *v[kMaxSeg];
     int len[kMaxSeg];
+    int cols[kMaxSeg];             // SegCols
+    int stream[kMaxSeg];           // rows read once per call: non-temporal loads
     int first_tile[kMaxSeg + 1];   // tiles before segment s; [n_seg] = total
     int n_seg;
 };
@@ -43,21 +55,28 @@ __device__ __forceinline__ void list_init(KeyList &L) {
         L.k[s] = nullptr;
         L.v[s] = nullptr;
         L.len[s] = 0;
+        L.cols[s] = kColsAll;
+        L.stream[s] = 0;
     }
 }
 
-// Appends n rows starting at (k, v); empty segments are dropped.  The
-// segment index only ever takes constant values after unrolling, so the
-// list stays in scalar registers.
-__device__ __forceinline__ void list_add(KeyList &L, const char *k, const char *v, int n) {
+// Appends n rows starting at (k, v); empty segments are dropped.  Tiles hold
+// TK keys (a list is built and walked with one TK).  The segment index only
+// takes constant values after unrolling, so the list stays in scalar
+// registers.
+template <int TK = kTileKeys>
+__device__ __forceinline__ void list_add(KeyList &L, const char *k, const char *v, int n, int cols = kColsAll,
+                                         bool stream = false) {
     if (n <= 0) return;
-    const int tiles = (n + kTileKeys - 1) / kTileKeys;
+    const int tiles = (n + TK - 1) / TK;
 #pragma unroll
     for (int s = 0; s < kMaxSeg; ++s) {
         if (s == L.n_seg) {
             L.k[s] = k;
             L.v[s] = v;
             L.len[s] = n;
+            L.cols[s] = cols;
+            L.stream[s] = stream ? 1 : 0;
             L.first_tile[s + 1] = L.first_tile[s] + tiles;
         } else if (s > L.n_seg) {
             L.first_tile[s + 1] = L.first_tile[s] + tiles;
@@ -74,14 +93,18 @@ __device__ __forceinline__ int list_tiles(const KeyList &L) {
     return t;
 }
 
-// Where tile t lies: base pointers of its first key and the number of keys.
+// Where tile t lies: base pointers of its first key, its valid key count and
+// which columns see it.
 struct TileRef {
     const char *k, *v;
     int n;
+    int cols;
+    int stream;
 };
 
+template <int TK = kTileKeys>
 __device__ __forceinline__ TileRef list_tile(const KeyList &L, int t, int row_bytes) {
-    TileRef r{L.k[0], L.v[0], 0};
+    TileRef r{L.k[0], L.v[0], 0, kColsAll, 0};
     int off = t;
 #pragma unroll
     for (int s = 0; s < kMaxSeg; ++s) {
@@ -90,12 +113,14 @@ __device__ __forceinline__ TileRef list_tile(const KeyList &L, int t, int row_by
             r.k = L.k[s];
             r.v = L.v[s];
             r.n = L.len[s];
+            r.cols = L.cols[s];
+            r.stream = L.stream[s];
         }
     }
-    const int t0 = off * kTileKeys;
+    const int t0 = off * TK;
     r.k += (size_t)t0 * row_bytes;
     r.v += (size_t)t0 * row_bytes;
-    r.n = min(kTileKeys, r.n - t0);
+    r.n = min(TK, r.n - t0);
     return r;
 }
 
@@ -104,7 +129,9 @@ struct WaveMfma {
     static constexpr int ROW = D * 2;               // bytes per K or V row
     static constexpr int NDS = D / 32;              // k-steps of q.k
     static constexpr int NDT = D / 16;              // 16-row d tiles of the output
-    static constexpr int NVU = D / 64;              // V units (4 keys x 8 d) per lane per tile
+    static constexpr int DG = D / 8;                // 16-byte groups of a row
+    static constexpr int UNITS = 4 * DG;            // V units (4 keys x 8 d) per tile
+    static constexpr int NVU = (UNITS + 63) / 64;   // V units per lane
     static constexpr int VROW = kTileKeys * 2 + 8;  // bytes per d row of the V^T tile (padded)
     static constexpr int LDS = D * VROW;            // V^T tile of one wave
 };
@@ -112,7 +139,7 @@ struct WaveMfma {
 // Registers of one tile in flight.
 template <int D>
 struct TileRegs {
-    u32x4_t k[2][WaveMfma<D>::NDS];   // [16-key half][k-step]
+    u32x4_t k[WaveMfma<D>::NDS];      // [k-step]
     u32x4_t v[WaveMfma<D>::NVU][4];   // [unit][key of the unit]
 };
 
@@ -121,48 +148,61 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t rows_rsrc(const char *base, in
     return __builtin_amdgcn_make_buffer_rsrc(const_cast<char *>(base), 0, bytes, 0x00020000);
 }
 
-template <int D>
-__device__ __forceinline__ void tile_load(const TileRef &t, TileRegs<D> &r) {
+// Cache policy of row loads: 2 = non-temporal (rows read once per call).
+template <int AUX>
+__device__ __forceinline__ u32x4_t row_load(__amdgpu_buffer_rsrc_t r, int off) {
+    return __builtin_bit_cast(u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, AUX));
+}
+
+template <int D, int AUX>
+__device__ __forceinline__ void tile_load_aux(const TileRef &t, TileRegs<D> &r) {
     using W = WaveMfma<D>;
     const int lane = threadIdx.x & 63, col = lane & 15, quad = lane >> 4;
     const __amdgpu_buffer_rsrc_t rk = rows_rsrc(t.k, t.n * W::ROW);
     const __amdgpu_buffer_rsrc_t rv = rows_rsrc(t.v, t.n * W::ROW);
-    static_for<0, 2>([&](auto h) {
-        const int off = (16 * h + col) * W::ROW + 16 * quad;
-        static_for<0, W::NDS>([&](auto st) {
-            r.k[h][st] = __builtin_amdgcn_raw_buffer_load_b128(rk, off + 64 * st, 0, 0);
-        });
-    });
+    const int koff = col * W::ROW + 16 * quad;
+    static_for<0, W::NDS>([&](auto st) { r.k[st] = row_load<AUX>(rk, koff + 64 * st); });
     static_for<0, W::NVU>([&](auto n) {
         const int u = lane + 64 * n;
-        const int dg = u % (D / 8), kq = u / (D / 8);
-        static_for<0, 4>([&](auto kk) {
-            r.v[n][kk] = __builtin_amdgcn_raw_buffer_load_b128(rv, (4 * kq + kk) * W::ROW + 16 * dg, 0, 0);
-        });
+        const int kq = u & 3, dg = u >> 2;   // unit: keys 4 kq .. 4 kq + 3, bytes 16 dg .. 16 dg + 15
+        if (u < W::UNITS) {
+            static_for<0, 4>([&](auto kk) { r.v[n][kk] = row_load<AUX>(rv, (4 * kq + kk) * W::ROW + 16 * dg); });
+        }
     });
 }
 
-// V^T tile: row d holds the tile's 32 keys (bf16) at byte 2 * key.
+template <int D>
+__device__ __forceinline__ void tile_load(const TileRef &t, TileRegs<D> &r) {
+    if (t.stream)
+        tile_load_aux<D, 2>(t, r);
+    else
+        tile_load_aux<D, 0>(t, r);
+}
+
+// V^T tile: row d holds the tile's 16 keys (bf16) at byte 2 * key.  The
+// four lanes of a unit row write one 32-byte row segment together.
 template <int D>
 __device__ __forceinline__ void tile_stage_vt(const TileRegs<D> &r, char *sVt) {
     using W = WaveMfma<D>;
     const int lane = threadIdx.x & 63;
     static_for<0, W::NVU>([&](auto n) {
         const int u = lane + 64 * n;
-        const int dg = u % (D / 8), kq = u / (D / 8);
-        static_for<0, 8>([&](auto j) {
-            constexpr int jj = decltype(j)::value;
-            constexpr uint32_t sel = (jj & 1) ? 0x07060302u : 0x05040100u;
-            const uint32_t lo = __builtin_amdgcn_perm(r.v[n][1][jj >> 1], r.v[n][0][jj >> 1], sel);
-            const uint32_t hi = __builtin_amdgcn_perm(r.v[n][3][jj >> 1], r.v[n][2][jj >> 1], sel);
-            *reinterpret_cast<u32x2_t *>(sVt + (8 * dg + jj) * W::VROW + 8 * kq) = u32x2_t{lo, hi};
-        });
+        const int kq = u & 3, dg = u >> 2;
+        if (u < W::UNITS) {
+            static_for<0, 8>([&](auto j) {
+                constexpr int jj = decltype(j)::value;
+                constexpr uint32_t sel = (jj & 1) ? 0x07060302u : 0x05040100u;
+                const uint32_t lo = __builtin_amdgcn_perm(r.v[n][1][jj >> 1], r.v[n][0][jj >> 1], sel);
+                const uint32_t hi = __builtin_amdgcn_perm(r.v[n][3][jj >> 1], r.v[n][2][jj >> 1], sel);
+                *reinterpret_cast<u32x2_t *>(sVt + (8 * dg + jj) * W::VROW + 8 * kq) = u32x2_t{lo, hi};
+            });
+        }
     });
 }
 
-// Streaming state of one wave.  Lane (quad, col) holds column col (head
-// col mod G): o[t][i] = O^T[16 t + 4 quad + i][col] relative to m; lsum is
-// this lane's share of the column's sum (the four quads add up at the end).
+// Streaming state of one wave.  Lane (quad, col) holds column col:
+// o[t][i] = O^T[16 t + 4 quad + i][col] relative to m; lsum is this lane's
+// share of the column's sum (the four quads add up at the end).
 template <int D>
 struct WaveState {
     f32x4_t o[WaveMfma<D>::NDT];
@@ -177,45 +217,50 @@ __device__ __forceinline__ void state_init(WaveState<D> &S) {
     S.lsum = 0.f;
 }
 
-// B operand of q.k: lane (quad, col) holds q[head col mod G][32 st + 8 quad ..+8].
-template <int D, int G>
-__device__ __forceinline__ void load_q_mfma(const char *q_heads, bf16x8_t (&qb)[WaveMfma<D>::NDS]) {
-    const int lane = threadIdx.x & 63, col = lane & 15, quad = lane >> 4;
-    const char *row = q_heads + (size_t)(col % G) * (D * 2);
+// B operand of q.k: lane (quad, col) holds q_row[32 st + 8 quad ..+8] of the
+// query row that column col stands for (zeros when q_row is null).
+template <int D>
+__device__ __forceinline__ void load_q_cols(const char *q_row, bf16x8_t (&qb)[WaveMfma<D>::NDS]) {
+    const int quad = (threadIdx.x & 63) >> 4;
     static_for<0, WaveMfma<D>::NDS>([&](auto st) {
-        qb[st] = __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const uint4 *>(row + (32 * st + 8 * quad) * 2));
+        uint4 w = make_uint4(0, 0, 0, 0);
+        if (q_row) w = *reinterpret_cast<const uint4 *>(q_row + (32 * st + 8 * quad) * 2);
+        qb[st] = __builtin_bit_cast(bf16x8_t, w);
     });
 }
+
+// Per-lane visibility of the three segment classes for this lane's column.
+struct ColMask {
+    bool all, clean, donor;
+    __device__ __forceinline__ bool on(int cols) const {
+        return cols == kColsAll ? all : (cols == kColsClean ? clean : donor);
+    }
+};
 
 // One tile: q.k, online softmax, p.v.  `kr` holds the tile's K rows; its V
 // rows have been staged in sVt by this wave.
 template <int D>
-__device__ __forceinline__ void tile_compute(const u32x4_t (&kr)[2][WaveMfma<D>::NDS], int n_valid,
+__device__ __forceinline__ void tile_compute(const u32x4_t (&kr)[WaveMfma<D>::NDS], int n_valid, bool col_on,
                                              const bf16x8_t (&qb)[WaveMfma<D>::NDS], float qk_scale,
                                              const char *sVt, WaveState<D> &S) {
     using W = WaveMfma<D>;
     const int lane = threadIdx.x & 63, col = lane & 15, quad = lane >> 4;
-    f32x4_t s[2];
-    static_for<0, 2>([&](auto h) {
-        s[h] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-        static_for<0, W::NDS>([&](auto st) {
-            s[h] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, kr[h][st]), qb[st], s[h], 0, 0, 0);
-        });
+    f32x4_t s = {0.f, 0.f, 0.f, 0.f};
+    static_for<0, W::NDS>([&](auto st) {
+        s = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, kr[st]), qb[st], s, 0, 0, 0);
     });
-    float x[2][4];
+    float x[4];
     float mt = -INFINITY;
-    static_for<0, 2>([&](auto h) {
-        static_for<0, 4>([&](auto i) {
-            const int key = 16 * h + 4 * quad + i;
-            x[h][i] = key < n_valid ? s[h][(int)i] * qk_scale : -INFINITY;
-            mt = fmaxf(mt, x[h][i]);
-        });
+    static_for<0, 4>([&](auto i) {
+        const int key = 4 * quad + i;
+        x[i] = (col_on && key < n_valid) ? s[(int)i] * qk_scale : -INFINITY;
+        mt = fmaxf(mt, x[i]);
     });
     mt = fmaxf(mt, __shfl_xor(mt, 16));
     mt = fmaxf(mt, __shfl_xor(mt, 32));
     // lazy rescale: a column moves its maximum only when a score exceeds it
     // by more than kSlack (weights stay <= 2^kSlack); every lane of a column
-    // takes the same decision
+    // takes the same decision, and other columns multiply by exactly 1
     const bool need = mt > S.m + kSlack;
     if (__any(need)) {
         const float mn = need ? fmaxf(S.m, mt) : S.m;
@@ -225,33 +270,29 @@ __device__ __forceinline__ void tile_compute(const u32x4_t (&kr)[2][WaveMfma<D>:
         S.m = mn;
     }
     const float ms = S.m == -INFINITY ? 0.f : S.m;
-    bf16x8_t ph, pl;
-    static_for<0, 2>([&](auto h) {
-        static_for<0, 4>([&](auto i) {
-            constexpr int jj = 4 * decltype(h)::value + decltype(i)::value;
-            const float p = fast_exp2(x[h][i] - ms);
-            S.lsum += p;
-            const __bf16 hb = (__bf16)p;
-            ph[jj] = hb;
-            pl[jj] = (__bf16)(p - (float)hb);
-        });
+    i16x4_t ph, pl;
+    static_for<0, 4>([&](auto i) {
+        const float p = fast_exp2(x[i] - ms);
+        S.lsum += p;
+        const __bf16 hb = (__bf16)p;
+        ph[(int)i] = __builtin_bit_cast(short, hb);
+        pl[(int)i] = __builtin_bit_cast(short, (__bf16)(p - (float)hb));
     });
-    // k-slot 8 quad + j of the p.v product is key 4 quad + j (j < 4) or
-    // 16 + 4 quad + (j - 4): the keys whose scores this lane holds
+    // k-slot 4 quad + i of the p.v product is key 4 quad + i: the keys whose
+    // scores this lane holds
     static_for<0, W::NDT>([&](auto t) {
-        const char *vrow = sVt + (16 * t + col) * W::VROW;
-        const uint2 va = *reinterpret_cast<const uint2 *>(vrow + 8 * quad);
-        const uint2 vb = *reinterpret_cast<const uint2 *>(vrow + 32 + 8 * quad);
-        const bf16x8_t vf = __builtin_bit_cast(bf16x8_t, make_uint4(va.x, va.y, vb.x, vb.y));
-        S.o[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, ph, S.o[t], 0, 0, 0);
-        S.o[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pl, S.o[t], 0, 0, 0);
+        const uint2 va = *reinterpret_cast<const uint2 *>(sVt + (16 * t + col) * W::VROW + 8 * quad);
+        const i16x4_t vf = __builtin_bit_cast(i16x4_t, va);
+        S.o[t] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(vf, ph, S.o[t], 0, 0, 0);
+        S.o[t] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(vf, pl, S.o[t], 0, 0, 0);
     });
 }
 
 // Stream tiles t = first, first + step, ... of the list through one wave.
 template <int D>
-__device__ __forceinline__ void wave_stream(const KeyList &L, int first, int step, const bf16x8_t (&qb)[WaveMfma<D>::NDS],
-                                            float qk_scale, char *sVt, WaveState<D> &S) {
+__device__ __forceinline__ void wave_stream(const KeyList &L, int first, int step, const ColMask &cm,
+                                            const bf16x8_t (&qb)[WaveMfma<D>::NDS], float qk_scale, char *sVt,
+                                            WaveState<D> &S) {
     const int n_tiles = list_tiles(L);
     int t = first;
     if (t >= n_tiles) return;
@@ -262,15 +303,16 @@ __device__ __forceinline__ void wave_stream(const KeyList &L, int first, int ste
         // V goes to LDS and K is kept aside, so the next tile's loads can be
         // issued into `r` before this tile is computed
         tile_stage_vt<D>(r, sVt);
-        u32x4_t kr[2][WaveMfma<D>::NDS];
-        static_for<0, 2>([&](auto h) { static_for<0, WaveMfma<D>::NDS>([&](auto st) { kr[h][st] = r.k[h][st]; }); });
+        u32x4_t kr[WaveMfma<D>::NDS];
+        static_for<0, WaveMfma<D>::NDS>([&](auto st) { kr[st] = r.k[st]; });
         const int n_valid = cur.n;
+        const bool col_on = cm.on(cur.cols);
         const int nt = t + step;
         if (nt < n_tiles) {
             cur = list_tile(L, nt, WaveMfma<D>::ROW);
             tile_load<D>(cur, r);
         }
-        tile_compute<D>(kr, n_valid, qb, qk_scale, sVt, S);
+        tile_compute<D>(kr, n_valid, col_on, qb, qk_scale, sVt, S);
         if (nt >= n_tiles) break;
         t = nt;
     }
@@ -283,10 +325,11 @@ __device__ __forceinline__ void state_finish(WaveState<D> &S) {
     S.lsum += __shfl_xor(S.lsum, 32);
 }
 
-// Merge the waves of a work group (each with its WaveState, finished) through
-// LDS and hand every group of four consecutive outputs of each head to
-// sink(h, d, M, L, O) -- M and L in base-2 units, O not yet divided by L.
-// `buf` needs kWaves * G * (D + 2) floats and may alias the V^T tiles.
+// Merge the waves of a work group (each with its WaveState, finished, the
+// same G heads in columns j mod G) through LDS and hand every group of four
+// consecutive outputs of each head to sink(h, d, M, L, O) -- M and L in
+// base-2 units, O not yet divided by L.  `buf` needs kWaves * G * (D + 2)
+// floats and may alias the V^T tiles.
 template <int D, int G, typename Sink>
 __device__ __forceinline__ void waves_merge(WaveState<D> &S, char *buf, Sink sink) {
     using W = WaveMfma<D>;
