@@ -14,11 +14,13 @@ Reported (one JSON line):
               it, donor span if a spliced cell reads a donor buffer, every
               cell's visible generated rows, out and lse);
   cell_steps_per_s   C * K / wall time;
-  roofline    bound "hbm": achieved = algorithmic bytes per launch / average
-              launch duration (HIP events on the launch stream, over the
-              timed region), peak 8000 GB/s, and the HBM traffic per launch
-              from the committed rocprofv3 counter summary when it was taken
-              on the current kernel source (else null);
+  roofline    bound "hbm": achieved = algorithmic bytes per call / average
+              call duration (HIP events on the launch stream, over the timed
+              region; a call is one launch of the per-cell kernel, or the
+              prompt launch plus the generated-row launch), peak 8000 GB/s,
+              and the HBM traffic per call from the committed rocprofv3
+              counter summary when it was taken on the current kernel source
+              (else null);
   cpu_baseline  the fp64 oracle timed on this host's cores on a stratified
               sample of the same workload's calls.
 
@@ -86,6 +88,15 @@ def call_bytes(w, layer: int, step: int, spliced_flags) -> int:
     return total
 
 
+def launch_kernels(w) -> str:
+    """Kernels one splice_decode_attn call launches on this workload (bf16):
+    prompts of at most 512 visible keys take the per-cell kernel, longer ones
+    the shared-prompt kernel followed by the generated-row kernel."""
+    if w.dtype != "bf16":
+        return "items_kernel"
+    return "cellwise_mfma_kernel" if w.prompt_len <= 512 else "prompt_wide_kernel + gen_merge_kernel"
+
+
 def spliced_flags(w, layer, step):
     return [layer >= L and step >= W for (L, W) in w.cells]
 
@@ -135,7 +146,7 @@ def cpu_baseline(w, seconds_cap: float = 30.0):
 def stored_traffic(w_name: str):
     """HBM bytes per launch from the committed rocprofv3 counter summary, if it
     was taken on the current kernel source and workload."""
-    path = os.path.join(PROFILES, f"attn_kernel_{w_name}_traffic.txt")
+    path = os.path.join(PROFILES, f"splice_decode_attn_{w_name}_traffic.txt")
     if not os.path.exists(path):
         return None, "no counter summary"
     fields = {}
@@ -267,7 +278,7 @@ def main():
     roofline = {"bound": "hbm", "achieved": round(per_launch_bytes / avg_launch_s / 1e9, 2),
                 "peak": HBM_PEAK_GBS, "unit": "GB/s",
                 "frac": round(per_launch_bytes / avg_launch_s / 1e9 / HBM_PEAK_GBS, 4),
-                "traffic": traffic, "kernel": "attn_kernel",
+                "traffic": traffic, "kernel": launch_kernels(w),
                 "bytes_per_launch": round(per_launch_bytes),
                 "avg_launch_us": round(avg_launch_s * 1e6, 3),
                 "traffic_source": traffic_src, "kernel_source_sha256_16": kernel_source_hash()}

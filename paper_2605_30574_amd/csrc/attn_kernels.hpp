@@ -463,7 +463,27 @@ __device__ void combine_cells(const AttnArgs &a, const int *list, int n, int g, 
 
 // Waves per SIMD the register allocation must allow: the bf16 streams fit 4
 // (128 VGPRs) at D <= 128 and 2 at D = 256.
-constexpr int waves_per_simd(int D) { return D <= 128 ? 4 : 2; }
+// Tiles each wave keeps in flight.  The per-cell kernel walks L2-resident
+// prompt tiles and generated rows in one chain: two in flight halve the
+// chain (D = 256 keeps one: a second tile set does not fit without
+// spilling).  The generated-row kernel streams HBM rows with one tile in
+// flight at 4 waves per SIMD, which measured faster than two at 3.
+constexpr int cellwise_depth(int D) { return D <= 128 ? 2 : 1; }
+constexpr int kGenDepth = 1;
+
+
+// Cache policy of row loads: normal.  Each K load instruction covers 64
+// bytes of 16 rows (the MFMA operand layout), so the other half of every
+// 128-byte line arrives with the next instruction; non-temporal loads, which
+// do not keep the line, measured slower here.
+constexpr int kLoadCached = 0;
+constexpr int kGenAux = kLoadCached;
+constexpr int kCellwiseAux = kLoadCached;
+
+// Waves per SIMD the register allocation must allow for the per-(cell, KV
+// head) streams: 4 (128 VGPRs) fit one tile in flight at D <= 128, 3 fit two;
+// D = 256 fits 2.
+constexpr int waves_per_simd(int D, int depth = 1) { return D <= 128 ? (depth > 1 ? 3 : 4) : 2; }
 
 // f32 inputs, one launch per call: blocks [0, n_prompt_items) are prompt
 // items (cell, KV head, prompt chunk), the rest generated-row items; the
@@ -517,10 +537,9 @@ __global__ __launch_bounds__(kThreads) void prompt_wide_kernel(AttnArgs a) {
     const int g = item / a.n_rb;
     const int lane = threadIdx.x & 63, col = lane & 15, quad = lane >> 4;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-    ColMask cm[X::RB];
     bf16x8_t qb[X::RB][X::NDS];
     int cell[X::RB], hh[X::RB];
-    int clean_here = 0, donor_here = 0;
+    bool ok[X::RB];
     // row groups of unspliced cells come first; a group never mixes classes
     const bool clean_group = rg < a.n_rg_clean;
     const int first_cell = clean_group ? 0 : a.n_clean;
@@ -529,20 +548,16 @@ __global__ __launch_bounds__(kThreads) void prompt_wide_kernel(AttnArgs a) {
     static_for<0, X::RB>([&](auto rb) {
         const int R = grp * X::ROWS + (wave * X::RB + rb) * 16 + col;
         const int cidx = first_cell + R / G;
-        const bool ok = cidx < end_cell;
-        cell[rb] = ok ? a.order[cidx] : 0;
+        ok[rb] = cidx < end_cell;
+        cell[rb] = ok[rb] ? a.order[cidx] : 0;
         hh[rb] = R % G;
-        const bool spl = ok && bit_set(a.spliced, cell[rb]);
-        cm[rb] = ColMask{ok, ok && !spl, spl && !a.zero_donor};
-        clean_here |= cm[rb].clean ? 1 : 0;
-        donor_here |= cm[rb].donor ? 1 : 0;
-        load_q_cols<D>(ok ? a.q + ((size_t)cell[rb] * a.Hq + (size_t)g * G + hh[rb]) * X::ROW : nullptr, qb[rb]);
+        load_q_cols<D>(ok[rb] ? a.q + ((size_t)cell[rb] * a.Hq + (size_t)g * G + hh[rb]) * X::ROW : nullptr,
+                       qb[rb]);
     });
-    // the span passes the work group needs: clean rows read the clean span,
-    // spliced rows the donor span (a ZERO splice reads none)
-    const bool any_clean = __builtin_amdgcn_readfirstlane(__syncthreads_or(clean_here)) != 0;
-    const bool any_donor = __builtin_amdgcn_readfirstlane(__syncthreads_or(donor_here)) != 0;
 
+    // the prompt chunk: clean before and after the span; the span from the
+    // clean cache (unspliced rows), the donor cache (spliced rows) or not at
+    // all (ZERO splice: its closed-form term is added by the merge)
     const int k0 = a.jp0 + pk * a.p_len;
     const int k1 = min(k0 + a.p_len, a.Tp);
     const size_t head = (size_t)g * a.Tp * X::ROW;
@@ -551,11 +566,11 @@ __global__ __launch_bounds__(kThreads) void prompt_wide_kernel(AttnArgs a) {
     KeyList L;
     list_init(L);
     list_add<X::TK>(L, ck + (size_t)k0 * X::ROW, cv + (size_t)k0 * X::ROW, pre1 - k0);
-    if (any_clean)
-        list_add<X::TK>(L, ck + (size_t)sp0 * X::ROW, cv + (size_t)sp0 * X::ROW, sp1 - sp0, kColsClean);
-    if (any_donor) {
+    if (clean_group) {
+        list_add<X::TK>(L, ck + (size_t)sp0 * X::ROW, cv + (size_t)sp0 * X::ROW, sp1 - sp0);
+    } else if (!a.zero_donor) {
         const char *dk = a.dk + head, *dv = a.dv + head;
-        list_add<X::TK>(L, dk + (size_t)sp0 * X::ROW, dv + (size_t)sp0 * X::ROW, sp1 - sp0, kColsDonor);
+        list_add<X::TK>(L, dk + (size_t)sp0 * X::ROW, dv + (size_t)sp0 * X::ROW, sp1 - sp0);
     }
     list_add<X::TK>(L, ck + (size_t)post0 * X::ROW, cv + (size_t)post0 * X::ROW, k1 - post0);
 
@@ -565,14 +580,14 @@ __global__ __launch_bounds__(kThreads) void prompt_wide_kernel(AttnArgs a) {
         S.m[rb] = -INFINITY;
         S.lsum[rb] = 0.f;
     });
-    wide_stream<D>(L, cm, qb, a.qk_scale, lds, S);
+    wide_stream<D>(L, qb, a.qk_scale, lds, S);
 
     char *part = reinterpret_cast<char *>(a.part);
     static_for<0, X::RB>([&](auto rb) {
         float l = S.lsum[rb];
         l += __shfl_xor(l, 16);
         l += __shfl_xor(l, 32);
-        if (cm[rb].all) {
+        if (ok[rb]) {
             char *slot = part + slot_off(a, cell[rb], g, pk);
             static_for<0, X::NDT>([&](auto t) {
                 *reinterpret_cast<f32x4_t *>(slot + (size_t)(hh[rb] * D + 16 * t + 4 * quad) * 4) = S.o[rb][t];
@@ -586,11 +601,11 @@ __global__ __launch_bounds__(kThreads) void prompt_wide_kernel(AttnArgs a) {
 }
 
 // Launch 2: one work group per (cell, KV head) streams the cell's generated
-// rows (four waves, interleaved tiles, non-temporal loads), merges its waves,
+// rows (four waves, interleaved tiles), merges its waves,
 // folds in the prompt partials of launch 1 in chunk order and then the ZERO
 // term (n_zero keys of score 0 and value 0), and writes out and lse.
 template <int D, int G>
-__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(waves_per_simd(D))))
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(waves_per_simd(D, kGenDepth))))
 void gen_merge_kernel(AttnArgs a) {
     using W = WaveMfma<D>;
     __shared__ __attribute__((aligned(16))) char buf[CellwiseLds<D, G>::BYTES];
@@ -603,11 +618,11 @@ void gen_merge_kernel(AttnArgs a) {
     const size_t goff = (((size_t)c * a.Hkv + g) * (size_t)a.cap + a.i0) * W::ROW;
     KeyList L;
     list_init(L);
-    list_add(L, a.gk + goff, a.gv + goff, a.n_gen, kColsAll, true);
+    list_add(L, a.gk + goff, a.gv + goff, a.n_gen);
     WaveState<D> S;
     state_init(S);
     const ColMask cm{true, true, true};
-    wave_stream<D>(L, wave, kWaves, cm, qb, a.qk_scale, buf + wave * W::LDS, S);
+    wave_stream<D, kGenDepth, kGenAux>(L, wave, kWaves, cm, qb, a.qk_scale, buf + wave * W::LDS, S);
     state_finish(S);
 
     const bool zero_term = a.zero_donor && bit_set(a.spliced, c) && a.sb > a.sa;
@@ -709,7 +724,7 @@ __global__ __launch_bounds__(kThreads) void cellwise_kernel(AttnArgs a) {
 // and the span segment exists whether or not the cell is spliced, so a
 // splice never moves a tile boundary.
 template <int D, int G>
-__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(waves_per_simd(D))))
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(waves_per_simd(D, cellwise_depth(D)))))
 void cellwise_mfma_kernel(AttnArgs a) {
     using W = WaveMfma<D>;
     __shared__ __attribute__((aligned(16))) char buf[CellwiseLds<D, G>::BYTES];
@@ -733,11 +748,11 @@ void cellwise_mfma_kernel(AttnArgs a) {
         list_add(L, a.ck + head + (size_t)a.sb * W::ROW, a.cv + head + (size_t)a.sb * W::ROW, a.Tp - a.sb);
     }
     const size_t goff = (((size_t)c * a.Hkv + g) * (size_t)a.cap + a.i0) * W::ROW;
-    list_add(L, a.gk + goff, a.gv + goff, a.n_gen, kColsAll, true);
+    list_add(L, a.gk + goff, a.gv + goff, a.n_gen);
     WaveState<D> S;
     state_init(S);
     const ColMask cm{true, true, true};
-    wave_stream<D>(L, wave, kWaves, cm, qb, a.qk_scale, buf + wave * W::LDS, S);
+    wave_stream<D, cellwise_depth(D), kCellwiseAux>(L, wave, kWaves, cm, qb, a.qk_scale, buf + wave * W::LDS, S);
     state_finish(S);
     const int nsv = a.sb - a.sa;
     const bool zero_term = zskip && nsv > 0;

@@ -120,6 +120,7 @@ constexpr int kMaxSlots = 64;              // partial results per (cell, KV head
 constexpr int kPromptItemsTarget = 512;    // f32 prompt items a default split aims for
 constexpr int kGenItemsTarget = 2048;      // f32 generated items a default split aims for
 constexpr int kWideItemsTarget = 512;      // bf16 prompt work groups a default split aims for
+constexpr int kWideMinChunk = 128;         // a default bf16 prompt chunk is at least this long
 
 // bf16 prompt kernel: 16-row MFMA blocks per wave (so that a wave's output
 // accumulators, RB * D / 4 registers, stay at 64) and rows per work group
@@ -172,9 +173,9 @@ inline int gen_chunk_target(const splice_shape &sh) {
     return t < 1 ? 1 : (t > kMaxChunks ? kMaxChunks : (int)t);
 }
 
-// Cut n keys into chunks.  Default: k = min(ceil(n / kMinChunk), target)
+// Cut n keys into chunks.  Default: k = min(ceil(n / min_chunk), target)
 // chunks of equal length rounded up to 64; split > 0 fixes the length.
-inline void cut(int n, int target, int split, int *k, int *len) {
+inline void cut(int n, int target, int split, int *k, int *len, int min_chunk = kMinChunk) {
     if (n <= 0) {
         *k = 0;
         *len = 64;
@@ -185,7 +186,7 @@ inline void cut(int n, int target, int split, int *k, int *len) {
         *k = ceil_div(n, split);
         return;
     }
-    int kk = ceil_div(n, kMinChunk);
+    int kk = ceil_div(n, min_chunk);
     if (kk > target) kk = target;
     *len = round_up(ceil_div(n, kk), 64);
     *k = ceil_div(n, *len);
@@ -223,7 +224,8 @@ inline AttnPlan plan_attn(const splice_shape &sh, const splice_call &call, int n
         p.n_prompt_items = p.n_gen_items = 0;
         return p;
     }
-    cut(p.geo.n_prompt, prompt_chunk_target(sh), call.split_keys, &p.n_p, &p.p_len);
+    cut(p.geo.n_prompt, prompt_chunk_target(sh), call.split_keys, &p.n_p, &p.p_len,
+        bf16_path(sh) ? kWideMinChunk : kMinChunk);
     if (bf16_path(sh)) {
         // the generated-row work group folds the prompt partials in itself
         p.n_g = 1;
@@ -261,14 +263,15 @@ inline WorkspaceLayout workspace_layout(const splice_shape &sh, int n_slots) {
 // default cut makes at most min(ceil(n / kMinChunk), target) chunks (each
 // chunk is at least n / that many keys long), and that bound grows with n;
 // a call sees at most T_p prompt keys and gen_capacity generated rows.
-inline int max_default_chunks(int n, int target) {
+inline int max_default_chunks(int n, int target, int min_chunk = kMinChunk) {
     if (n <= 0) return 0;
-    const int k = ceil_div(n, kMinChunk);
+    const int k = ceil_div(n, min_chunk);
     return k < target ? k : target;
 }
 
 inline int worst_default_slots(const splice_shape &sh) {
-    const int prompt = max_default_chunks(sh.prompt_len, prompt_chunk_target(sh));
+    const int prompt = max_default_chunks(sh.prompt_len, prompt_chunk_target(sh),
+                                          bf16_path(sh) ? kWideMinChunk : kMinChunk);
     return bf16_path(sh) ? prompt : prompt + max_default_chunks(sh.gen_capacity, gen_chunk_target(sh));
 }
 

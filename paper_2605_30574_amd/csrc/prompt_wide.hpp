@@ -93,10 +93,12 @@ struct WideState {
     float lsum[Wide<D>::RB];
 };
 
-// One staged tile for this wave's RB row blocks.  on[rb]: the tile's
-// segment is visible to this lane's row of block rb.
+// One staged tile for this wave's RB row blocks.  A work group's rows all
+// belong to one class (unspliced or spliced cells), so every tile of its list
+// is visible to every row; rows past the last cell compute values that are
+// never stored.  Only a partial tile (n_valid < TK) masks keys.
 template <int D>
-__device__ __forceinline__ void wide_compute(const char *buf, int n_valid, const bool (&on)[Wide<D>::RB],
+__device__ __forceinline__ void wide_compute(const char *buf, int n_valid,
                                              const bf16x8_t (&qb)[Wide<D>::RB][Wide<D>::NDS], float qk_scale,
                                              WideState<D> &S) {
     using X = Wide<D>;
@@ -120,14 +122,18 @@ __device__ __forceinline__ void wide_compute(const char *buf, int n_valid, const
     bf16x8_t ph[X::RB], pl[X::RB];
     static_for<0, X::RB>([&](auto rb) {
         float x[2][4];
-        float mt = -INFINITY;
         static_for<0, 2>([&](auto h) {
-            static_for<0, 4>([&](auto i) {
-                const int key = 16 * h + 4 * quad + i;
-                x[h][i] = (on[rb] && key < n_valid) ? s[rb][h][(int)i] * qk_scale : -INFINITY;
-                mt = fmaxf(mt, x[h][i]);
-            });
+            static_for<0, 4>([&](auto i) { x[h][i] = s[rb][h][(int)i] * qk_scale; });
         });
+        if (n_valid < X::TK) {   // uniform: only the last tile of a segment
+            static_for<0, 2>([&](auto h) {
+                static_for<0, 4>([&](auto i) {
+                    if (16 * h + 4 * quad + i >= n_valid) x[h][i] = -INFINITY;
+                });
+            });
+        }
+        float mt = -INFINITY;
+        static_for<0, 2>([&](auto h) { static_for<0, 4>([&](auto i) { mt = fmaxf(mt, x[h][i]); }); });
         mt = fmaxf(mt, __shfl_xor(mt, 16));
         mt = fmaxf(mt, __shfl_xor(mt, 32));
         const bool need = mt > S.m[rb] + kSlack;
@@ -174,9 +180,8 @@ constexpr int wide_depth() { return D <= 128 ? 3 : 2; }
 // sets are only ever indexed by constants.  Called by all threads of the
 // work group.
 template <int D>
-__device__ __forceinline__ void wide_stream(const KeyList &L, const ColMask (&cm)[Wide<D>::RB],
-                                            const bf16x8_t (&qb)[Wide<D>::RB][Wide<D>::NDS], float qk_scale,
-                                            char *lds, WideState<D> &S) {
+__device__ __forceinline__ void wide_stream(const KeyList &L, const bf16x8_t (&qb)[Wide<D>::RB][Wide<D>::NDS],
+                                            float qk_scale, char *lds, WideState<D> &S) {
     using X = Wide<D>;
     constexpr int DEPTH = wide_depth<D>();
     const int n_tiles = list_tiles(L);
@@ -184,10 +189,8 @@ __device__ __forceinline__ void wide_stream(const KeyList &L, const ColMask (&cm
     WideRegs<D> r[DEPTH];
     TileRef ref[DEPTH];
     static_for<0, DEPTH>([&](auto i) {
-        if (i < n_tiles) {
-            ref[i] = list_tile<X::TK>(L, i, X::ROW);
-            wide_fetch<D>(ref[i], r[i]);
-        }
+        ref[i] = list_tile_or_empty<X::TK>(L, i, n_tiles, X::ROW);
+        wide_fetch<D>(ref[i], r[i]);
     });
     wide_stage<D>(r[0], lds);
     __syncthreads();
@@ -195,15 +198,15 @@ __device__ __forceinline__ void wide_stream(const KeyList &L, const ColMask (&cm
         static_for<0, DEPTH>([&](auto j) {
             constexpr int jn = (decltype(j)::value + 1) % DEPTH;
             const int t = base + j;
-            if (t < n_tiles) {
-                const TileRef cur = ref[j];
-                if (t + DEPTH < n_tiles) {   // registers of tile t are free: refill them
-                    ref[j] = list_tile<X::TK>(L, t + DEPTH, X::ROW);
-                    wide_fetch<D>(ref[j], r[j]);
-                }
-                bool on[X::RB];
-                static_for<0, X::RB>([&](auto rb) { on[rb] = cm[rb].on(cur.cols); });
-                wide_compute<D>(lds + (t & 1) * X::BUF, cur.n, on, qb, qk_scale, S);
+            const bool live = t < n_tiles;   // false only in the last round
+            const TileRef cur = ref[j];
+            // registers of tile t are free (staged last iteration): refill them
+            // with tile t + DEPTH, or an empty tile past the end, on every
+            // path, so the count of loads in flight never depends on `live`
+            ref[j] = list_tile_or_empty<X::TK>(L, t + DEPTH, n_tiles, X::ROW);
+            wide_fetch<D>(ref[j], r[j]);
+            if (live) {
+                wide_compute<D>(lds + (t & 1) * X::BUF, cur.n, qb, qk_scale, S);
                 if (t + 1 < n_tiles) wide_stage<D>(r[jn], lds + ((t + 1) & 1) * X::BUF);
                 __syncthreads();   // the next buffer is staged; nobody reads this one any more
             }

@@ -41,7 +41,6 @@ struct KeyList {
     const char *v[kMaxSeg];
     int len[kMaxSeg];
     int cols[kMaxSeg];             // SegCols
-    int stream[kMaxSeg];           // rows read once per call: non-temporal loads
     int first_tile[kMaxSeg + 1];   // tiles before segment s; [n_seg] = total
     int n_seg;
 };
@@ -56,7 +55,6 @@ __device__ __forceinline__ void list_init(KeyList &L) {
         L.v[s] = nullptr;
         L.len[s] = 0;
         L.cols[s] = kColsAll;
-        L.stream[s] = 0;
     }
 }
 
@@ -65,8 +63,7 @@ __device__ __forceinline__ void list_init(KeyList &L) {
 // takes constant values after unrolling, so the list stays in scalar
 // registers.
 template <int TK = kTileKeys>
-__device__ __forceinline__ void list_add(KeyList &L, const char *k, const char *v, int n, int cols = kColsAll,
-                                         bool stream = false) {
+__device__ __forceinline__ void list_add(KeyList &L, const char *k, const char *v, int n, int cols = kColsAll) {
     if (n <= 0) return;
     const int tiles = (n + TK - 1) / TK;
 #pragma unroll
@@ -76,7 +73,6 @@ __device__ __forceinline__ void list_add(KeyList &L, const char *k, const char *
             L.v[s] = v;
             L.len[s] = n;
             L.cols[s] = cols;
-            L.stream[s] = stream ? 1 : 0;
             L.first_tile[s + 1] = L.first_tile[s] + tiles;
         } else if (s > L.n_seg) {
             L.first_tile[s + 1] = L.first_tile[s] + tiles;
@@ -99,12 +95,11 @@ struct TileRef {
     const char *k, *v;
     int n;
     int cols;
-    int stream;
 };
 
 template <int TK = kTileKeys>
 __device__ __forceinline__ TileRef list_tile(const KeyList &L, int t, int row_bytes) {
-    TileRef r{L.k[0], L.v[0], 0, kColsAll, 0};
+    TileRef r{L.k[0], L.v[0], 0, kColsAll};
     int off = t;
 #pragma unroll
     for (int s = 0; s < kMaxSeg; ++s) {
@@ -114,7 +109,6 @@ __device__ __forceinline__ TileRef list_tile(const KeyList &L, int t, int row_by
             r.v = L.v[s];
             r.n = L.len[s];
             r.cols = L.cols[s];
-            r.stream = L.stream[s];
         }
     }
     const int t0 = off * TK;
@@ -122,6 +116,17 @@ __device__ __forceinline__ TileRef list_tile(const KeyList &L, int t, int row_by
     r.v += (size_t)t0 * row_bytes;
     r.n = min(TK, r.n - t0);
     return r;
+}
+
+// A tile reference that loads nothing: its buffer range is empty, so every
+// row load returns 0 without a memory access.  Issuing loads for it keeps the
+// number of loads in flight the same on every path, which lets the compiler
+// wait for exactly the tile it needs instead of for all of them.
+__device__ __forceinline__ TileRef empty_tile(const KeyList &L) { return TileRef{L.k[0], L.v[0], 0, kColsAll}; }
+
+template <int TK = kTileKeys>
+__device__ __forceinline__ TileRef list_tile_or_empty(const KeyList &L, int t, int n_tiles, int row_bytes) {
+    return t < n_tiles ? list_tile<TK>(L, t, row_bytes) : empty_tile(L);
 }
 
 template <int D>
@@ -148,7 +153,7 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t rows_rsrc(const char *base, in
     return __builtin_amdgcn_make_buffer_rsrc(const_cast<char *>(base), 0, bytes, 0x00020000);
 }
 
-// Cache policy of row loads: 2 = non-temporal (rows read once per call).
+// Row load with cache policy AUX (0 normal, 2 non-temporal).
 template <int AUX>
 __device__ __forceinline__ u32x4_t row_load(__amdgpu_buffer_rsrc_t r, int off) {
     return __builtin_bit_cast(u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, AUX));
@@ -171,13 +176,6 @@ __device__ __forceinline__ void tile_load_aux(const TileRef &t, TileRegs<D> &r) 
     });
 }
 
-template <int D>
-__device__ __forceinline__ void tile_load(const TileRef &t, TileRegs<D> &r) {
-    if (t.stream)
-        tile_load_aux<D, 2>(t, r);
-    else
-        tile_load_aux<D, 0>(t, r);
-}
 
 // V^T tile: row d holds the tile's 16 keys (bf16) at byte 2 * key.  The
 // four lanes of a unit row write one 32-byte row segment together.
@@ -288,33 +286,40 @@ __device__ __forceinline__ void tile_compute(const u32x4_t (&kr)[WaveMfma<D>::ND
     });
 }
 
-// Stream tiles t = first, first + step, ... of the list through one wave.
-template <int D>
+// Stream tiles t = first, first + step, ... of the list through one wave,
+// keeping DEPTH tiles in flight: when tile t is computed, the loads of the
+// next DEPTH - 1 tiles are outstanding.  The loop is unrolled DEPTH times so
+// the register sets are only ever indexed by constants.  AUX is the cache
+// policy of every row load (0 normal, 2 non-temporal); it is a constant so
+// that every path issues the same loads.
+template <int D, int DEPTH, int AUX>
 __device__ __forceinline__ void wave_stream(const KeyList &L, int first, int step, const ColMask &cm,
                                             const bf16x8_t (&qb)[WaveMfma<D>::NDS], float qk_scale, char *sVt,
                                             WaveState<D> &S) {
     const int n_tiles = list_tiles(L);
-    int t = first;
-    if (t >= n_tiles) return;
-    TileRegs<D> r;
-    TileRef cur = list_tile(L, t, WaveMfma<D>::ROW);
-    tile_load<D>(cur, r);
-    for (;;) {
-        // V goes to LDS and K is kept aside, so the next tile's loads can be
-        // issued into `r` before this tile is computed
-        tile_stage_vt<D>(r, sVt);
-        u32x4_t kr[WaveMfma<D>::NDS];
-        static_for<0, WaveMfma<D>::NDS>([&](auto st) { kr[st] = r.k[st]; });
-        const int n_valid = cur.n;
-        const bool col_on = cm.on(cur.cols);
-        const int nt = t + step;
-        if (nt < n_tiles) {
-            cur = list_tile(L, nt, WaveMfma<D>::ROW);
-            tile_load<D>(cur, r);
-        }
-        tile_compute<D>(kr, n_valid, col_on, qb, qk_scale, sVt, S);
-        if (nt >= n_tiles) break;
-        t = nt;
+    if (first >= n_tiles) return;
+    TileRegs<D> r[DEPTH];
+    TileRef ref[DEPTH];
+    static_for<0, DEPTH>([&](auto i) {
+        ref[i] = list_tile_or_empty(L, first + i * step, n_tiles, WaveMfma<D>::ROW);
+        tile_load_aux<D, AUX>(ref[i], r[i]);
+    });
+    for (int base = first; base < n_tiles; base += DEPTH * step) {
+        static_for<0, DEPTH>([&](auto j) {
+            const int t = base + j * step;
+            const bool live = t < n_tiles;   // false only in the last round
+            // V goes to LDS and K is kept aside, so the loads of tile
+            // t + DEPTH * step are issued into these registers before the tile
+            // is computed.  The loads are issued on every path (an empty tile
+            // past the end), so the count in flight never depends on `live`.
+            if (live) tile_stage_vt<D>(r[j], sVt);
+            u32x4_t kr[WaveMfma<D>::NDS];
+            static_for<0, WaveMfma<D>::NDS>([&](auto st) { kr[st] = r[j].k[st]; });
+            const TileRef cur = ref[j];
+            ref[j] = list_tile_or_empty(L, t + DEPTH * step, n_tiles, WaveMfma<D>::ROW);
+            tile_load_aux<D, AUX>(ref[j], r[j]);
+            if (live) tile_compute<D>(kr, cur.n, cm.on(cur.cols), qb, qk_scale, sVt, S);
+        });
     }
 }
 
