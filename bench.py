@@ -16,8 +16,7 @@ Reported (one JSON line):
   cell_steps_per_s   C * K / wall time;
   roofline    bound "hbm": achieved = algorithmic bytes per call / average
               call duration (HIP events on the launch stream, over the timed
-              region; a call is one launch of the per-cell kernel, or the
-              prompt launch plus the generated-row launch), peak 8000 GB/s,
+              region; a call is one kernel launch), peak 8000 GB/s,
               and the HBM traffic per call from the committed rocprofv3
               counter summary when it was taken on the current kernel source
               (else null);
@@ -89,12 +88,11 @@ def call_bytes(w, layer: int, step: int, spliced_flags) -> int:
 
 
 def launch_kernels(w) -> str:
-    """Kernels one splice_decode_attn call launches on this workload (bf16):
-    prompts of at most 512 visible keys take the per-cell kernel, longer ones
-    the shared-prompt kernel followed by the generated-row kernel."""
+    """The kernel one splice_decode_attn call launches on this workload: bf16
+    calls launch the one kernel of shared-prompt and generated-row items."""
     if w.dtype != "bf16":
-        return "items_kernel"
-    return "cellwise_mfma_kernel" if w.prompt_len <= 512 else "prompt_wide_kernel + gen_merge_kernel"
+        return "cellwise_kernel" if w.prompt_len <= 512 else "items_kernel"
+    return "fused_kernel"
 
 
 def spliced_flags(w, layer, step):

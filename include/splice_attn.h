@@ -58,7 +58,7 @@ extern "C" {
 #define SPLICE_API
 #endif
 
-#define SPLICE_ABI_VERSION 1
+#define SPLICE_ABI_VERSION 2
 #define SPLICE_MAX_CELLS 256
 
 typedef enum {
@@ -97,6 +97,11 @@ typedef struct {
     float scale;           /* softmax scale applied to q.k                            */
     int32_t split_keys;    /* keys per work item, 0 = library default; else a
                               multiple of 64 in [64, 65536] (tuning and tests)        */
+    int32_t merge_wait;    /* bf16 calls with prompt items: how many times a
+                              generated-row item polls for the prompt partials of
+                              its (cell, KV head) before it leaves the merge to
+                              the last item to finish; 0 = library default
+                              (about 16 ms), < 0 = never poll (tests)             */
 } splice_call;
 
 /* ABI version this library was built with (SPLICE_ABI_VERSION). */

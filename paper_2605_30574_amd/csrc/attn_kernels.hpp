@@ -24,6 +24,7 @@ struct AttnArgs {
     int n_p, p_len, n_g, g_len, n_slots, slot_floats;
     int n_rb, n_prompt_items, n_clean;
     int n_rg_clean;   // bf16 prompt row groups of unspliced cells (the rest: spliced cells)
+    int wait_polls;   // bf16 generated-row items: most polls for the prompt partials
     float qk_scale;   // scale * log2(e)
     uint32_t spliced[SPLICE_MAX_CELLS / 32];
     uint8_t order[SPLICE_MAX_CELLS];   // clean cells, then spliced cells
@@ -91,13 +92,6 @@ struct Lds {
     static constexpr int MERGE = kWaves * 4 * G * (D + 1) * 4 + kWaves * G * 4;
     static constexpr int STAGE = 2 * kMaxSlots * kRowBlock * 4;
     static constexpr int BYTES = cmax(MERGE, STAGE);
-};
-
-// LDS of the bf16 per-(cell, KV head) kernels: one V^T tile per wave, then
-// the wave merge.
-template <int D, int G>
-struct CellwiseLds {
-    static constexpr int BYTES = cmax(kWaves * WaveMfma<D>::LDS, kWaves * G * (D + 2) * 4);
 };
 
 // Maximum over the row groups of a wave of a value that is the same in all
@@ -360,6 +354,13 @@ __device__ void prompt_item_valu(const AttnArgs &a, int c, int g, int pk, char *
 // them in slot order with a log-sum-exp combine, adds the ZERO term, writes
 // out and lse, and re-arms the counter.  No cache-wide write-back or
 // invalidate is needed, so the cached tiles of other items survive.
+//
+// The combine of one (row, four outputs) is fixed: M = the maximum of the
+// slots' m (and 0 with a ZERO term); L starts at the ZERO term
+// n_zero 2^-M (or 0); then slot k = 0, 1, ... adds l_k 2^(m_k - M) to L and
+// o_k 2^(m_k - M) to O with one fused multiply-add per value; out = O / L.
+// Every merge site below follows it, so a result does not depend on which
+// item merged it.
 
 __device__ __forceinline__ void stores_performed() {
     __builtin_amdgcn_s_waitcnt(0);   // every outstanding memory operation of this lane is done
@@ -372,10 +373,27 @@ __device__ __forceinline__ bool arrive(const AttnArgs &a, int c, int g) {
     return prev == a.n_slots - 1;
 }
 
+__device__ __forceinline__ void fold_slot(float mk, float lk, f32x4_t ok, float M, float &L, f32x4_t &O) {
+    const float f = fast_exp2(mk - M);
+    L = fmaf(lk, f, L);
+    O.x = fmaf(ok.x, f, O.x);
+    O.y = fmaf(ok.y, f, O.y);
+    O.z = fmaf(ok.z, f, O.z);
+    O.w = fmaf(ok.w, f, O.w);
+}
+
+__device__ __forceinline__ bool has_zero_term(const AttnArgs &a, int c) {
+    return a.zero_donor && bit_set(a.spliced, c) && a.sb > a.sa;
+}
+
+__device__ __forceinline__ void write_row(const AttnArgs &a, int row, int d, int D, float M, float L, f32x4_t O) {
+    *reinterpret_cast<f32x4_t *>(a.out + (size_t)row * D + d) = O * (1.f / L);
+    if (d == 0) a.lse[row] = (M + log2f(L)) * kLn2;
+}
+
 // Merge the partial results of cells list[0..n) of KV head g.  One round of
 // loads stages every (m, l) in LDS; then each thread owns up to kMergeUnits
-// groups of four consecutive outputs and loads them two slots at a time, so
-// a merge costs a few memory round trips whatever the cell count.
+// groups of four consecutive outputs and loads them two slots at a time.
 constexpr int kMergeUnits = 4;
 
 template <int D, int G>
@@ -408,7 +426,7 @@ __device__ void combine_cells(const AttnArgs &a, const int *list, int n, int g, 
             const int c = list[i];
             sm_off[b] = i * per_cell + h;
             base[b] = slot_off(a, c, g, 0) + (uint32_t)(h * D + d) * 4u;
-            const bool zero_term = a.zero_donor && bit_set(a.spliced, c) && a.sb > a.sa;
+            const bool zero_term = has_zero_term(a, c);
             float mx = zero_term ? 0.f : -INFINITY;
             for (int k = 0; k < a.n_slots; ++k) mx = fmaxf(mx, s_m[sm_off[b] + k * G]);
             M[b] = mx;
@@ -425,12 +443,8 @@ __device__ void combine_cells(const AttnArgs &a, const int *list, int n, int g, 
             }
 #pragma unroll
             for (int b = 0; b < kMergeUnits; ++b) {
-                const float f0 = fast_exp2(s_m[sm_off[b] + k * G] - M[b]);
-                const float f1 = fast_exp2(s_m[sm_off[b] + (k + 1) * G] - M[b]);
-                L[b] = fmaf(s_l[sm_off[b] + k * G], f0, L[b]);
-                L[b] = fmaf(s_l[sm_off[b] + (k + 1) * G], f1, L[b]);
-                O[b] += v0[b] * f0;
-                O[b] += v1[b] * f1;
+                fold_slot(s_m[sm_off[b] + k * G], s_l[sm_off[b] + k * G], v0[b], M[b], L[b], O[b]);
+                fold_slot(s_m[sm_off[b] + (k + 1) * G], s_l[sm_off[b] + (k + 1) * G], v1[b], M[b], L[b], O[b]);
             }
         }
         if (k < a.n_slots) {
@@ -438,11 +452,8 @@ __device__ void combine_cells(const AttnArgs &a, const int *list, int n, int g, 
 #pragma unroll
             for (int b = 0; b < kMergeUnits; ++b) v0[b] = part_load4(r, base[b] + (uint32_t)k * slot_bytes);
 #pragma unroll
-            for (int b = 0; b < kMergeUnits; ++b) {
-                const float f0 = fast_exp2(s_m[sm_off[b] + k * G] - M[b]);
-                L[b] = fmaf(s_l[sm_off[b] + k * G], f0, L[b]);
-                O[b] += v0[b] * f0;
-            }
+            for (int b = 0; b < kMergeUnits; ++b)
+                fold_slot(s_m[sm_off[b] + k * G], s_l[sm_off[b] + k * G], v0[b], M[b], L[b], O[b]);
         }
 #pragma unroll
         for (int b = 0; b < kMergeUnits; ++b) {
@@ -450,9 +461,7 @@ __device__ void combine_cells(const AttnArgs &a, const int *list, int n, int g, 
             if (u < total) {
                 const int i = u / UPC, rem = u % UPC;
                 const int h = rem / (D / 4), d = 4 * (rem % (D / 4));
-                const int row = list[i] * a.Hq + g * G + h;
-                *reinterpret_cast<f32x4_t *>(a.out + (size_t)row * D + d) = O[b] * (1.f / L[b]);
-                if (d == 0) a.lse[row] = (M[b] + log2f(L[b])) * kLn2;
+                write_row(a, list[i] * a.Hq + g * G + h, d, D, M[b], L[b], O[b]);
             }
         }
     }
@@ -461,29 +470,12 @@ __device__ void combine_cells(const AttnArgs &a, const int *list, int n, int g, 
                            __HIP_MEMORY_SCOPE_AGENT);
 }
 
-// Waves per SIMD the register allocation must allow: the bf16 streams fit 4
-// (128 VGPRs) at D <= 128 and 2 at D = 256.
-// Tiles each wave keeps in flight.  The per-cell kernel walks L2-resident
-// prompt tiles and generated rows in one chain: two in flight halve the
-// chain (D = 256 keeps one: a second tile set does not fit without
-// spilling).  The generated-row kernel streams HBM rows with one tile in
-// flight at 4 waves per SIMD, which measured faster than two at 3.
-constexpr int cellwise_depth(int D) { return D <= 128 ? 2 : 1; }
-constexpr int kGenDepth = 1;
-
-
 // Cache policy of row loads: normal.  Each K load instruction covers 64
 // bytes of 16 rows (the MFMA operand layout), so the other half of every
 // 128-byte line arrives with the next instruction; non-temporal loads, which
 // do not keep the line, measured slower here.
 constexpr int kLoadCached = 0;
 constexpr int kGenAux = kLoadCached;
-constexpr int kCellwiseAux = kLoadCached;
-
-// Waves per SIMD the register allocation must allow for the per-(cell, KV
-// head) streams: 4 (128 VGPRs) fit one tile in flight at D <= 128, 3 fit two;
-// D = 256 fits 2.
-constexpr int waves_per_simd(int D, int depth = 1) { return D <= 128 ? (depth > 1 ? 3 : 4) : 2; }
 
 // f32 inputs, one launch per call: blocks [0, n_prompt_items) are prompt
 // items (cell, KV head, prompt chunk), the rest generated-row items; the
@@ -521,32 +513,79 @@ __global__ __launch_bounds__(kThreads) void items_kernel(AttnArgs a) {
 
 // ------------------------------------------------------- bf16, long prompts
 //
-// Launch 1: the shared-prompt contraction (prompt_wide.hpp).  Work group =
-// (KV head, group of Wide<D>::ROWS rows, prompt chunk); a group holds rows of
-// unspliced cells only or of spliced cells only.  Every row it owns gets one
-// partial result (o, m, l) for the chunk, stored with plain stores: launch 2
-// runs after this kernel has completed, which makes them visible.
+// One launch per call.  Blocks [0, n_prompt_items) are shared-prompt items
+// (prompt_wide.hpp): work group = (KV head, group of Wide::ROWS rows, prompt
+// chunk), where the rows of a KV head are the (cell, q head) pairs of every
+// cell, unspliced cells first, and a group holds rows of one class only.
+// Each K/V tile of the chunk is staged in LDS once for all of the group's
+// rows, and every row gets one partial result.  The other blocks are
+// generated-row items: one work group per (cell, KV head) streams the cell's
+// generated rows (four waves, interleaved tiles) and merges its waves into
+// one more partial.  Every item then counts itself on the (cell, KV head)
+// pairs it fed; the item that completes a pair merges its partials (slot
+// order: prompt chunks, then the generated rows; then the ZERO term) and
+// writes out and lse.  Prompt and generated work of different cells overlap
+// in the one grid.
+
+template <int D>
+constexpr int fused_row_blocks() { return splice::fused_row_blocks(D); }
+
+// Default bound of a generated-row item's wait for the prompt partials: a
+// poll is one agent-scope load (about a microsecond under load) plus a short
+// sleep, so 16384 polls stay around 16 ms -- far beyond any prompt item.
+constexpr int kDefaultWaitPolls = 16384;
+
+// Tiles in flight: the prompt items' register ring and each generated-row
+// wave.  Both fit the register budget of fused_waves_per_simd.
+template <int D>
+constexpr int fused_prompt_depth() { return D <= 128 ? 3 : 2; }
+template <int D>
+constexpr int fused_gen_depth() { return D <= 128 ? 2 : 1; }
+constexpr int fused_waves_per_simd(int D) { return D <= 128 ? 3 : 2; }
+
 template <int D, int G>
-__global__ __launch_bounds__(kThreads) void prompt_wide_kernel(AttnArgs a) {
-    using X = Wide<D>;
-    __shared__ __attribute__((aligned(16))) char lds[X::LDS];
-    int item = blockIdx.x;
-    const int pk = item % a.n_p;
-    item /= a.n_p;
-    const int rg = item % a.n_rb;
-    const int g = item / a.n_rb;
+struct FusedLds {
+    static constexpr int PROMPT = Wide<D, fused_row_blocks<D>()>::LDS;
+    static constexpr int WAVE_MERGE = kWaves * G * (D + 2) * 4;                // waves_merge buffer
+    static constexpr int GEN = cmax(kWaves * WaveMfma<D>::LDS,                  // V^T tiles
+                                    WAVE_MERGE + 2 * kMaxSlots * G * 4);        // + prompt slots' (m, l)
+    static constexpr int MERGE = 2 * kRowBlock * kMaxSlots * 4;                 // combine_cells staging
+    static constexpr int BYTES = cmax(cmax(PROMPT, GEN), MERGE);
+};
+
+// Most cells one item can complete: the cells of one row group.
+template <int D, int G>
+constexpr int fused_max_merge() { return Wide<D, fused_row_blocks<D>()>::ROWS / G; }
+
+// Each item returns its KV head and leaves in s_list the count and the list
+// of the cells it completed.
+//
+// Block b of the prompt part serves unit u = (KV head, chunk) and row group
+// rg with b mod 8 = u mod 8: work groups are handed to the eight XCDs in
+// turn, so every row group of a unit runs on one XCD and the unit's tiles
+// come from that XCD's L2 after the first read.  Blocks with u past the
+// last unit (a grid padded to whole rounds of eight) do nothing.
+template <int D, int G>
+__device__ int fused_prompt_item(const AttnArgs &a, int item, char *lds, int *s_list) {
+    constexpr int RB = fused_row_blocks<D>();
+    using X = Wide<D, RB>;
+    const int rg = (item / splice::kXcds) % a.n_rb;
+    const int u = (item / splice::kXcds / a.n_rb) * splice::kXcds + item % splice::kXcds;
+    if (u >= a.n_p * a.Hkv) return 0;   // s_list[0] stays 0: nothing to merge
+    const int pk = u % a.n_p;
+    const int g = u / a.n_p;
     const int lane = threadIdx.x & 63, col = lane & 15, quad = lane >> 4;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-    bf16x8_t qb[X::RB][X::NDS];
-    int cell[X::RB], hh[X::RB];
-    bool ok[X::RB];
+    bf16x8_t qb[RB][X::NDS];
+    int cell[RB], hh[RB];
+    bool ok[RB];
     // row groups of unspliced cells come first; a group never mixes classes
     const bool clean_group = rg < a.n_rg_clean;
     const int first_cell = clean_group ? 0 : a.n_clean;
     const int end_cell = clean_group ? a.n_clean : a.C;
     const int grp = clean_group ? rg : rg - a.n_rg_clean;
-    static_for<0, X::RB>([&](auto rb) {
-        const int R = grp * X::ROWS + (wave * X::RB + rb) * 16 + col;
+    static_for<0, RB>([&](auto rb) {
+        const int R = grp * X::ROWS + (wave * RB + rb) * 16 + col;
         const int cidx = first_cell + R / G;
         ok[rb] = cidx < end_cell;
         cell[rb] = ok[rb] ? a.order[cidx] : 0;
@@ -574,43 +613,54 @@ __global__ __launch_bounds__(kThreads) void prompt_wide_kernel(AttnArgs a) {
     }
     list_add<X::TK>(L, ck + (size_t)post0 * X::ROW, cv + (size_t)post0 * X::ROW, k1 - post0);
 
-    WideState<D> S;
-    static_for<0, X::RB>([&](auto rb) {
+    WideState<D, RB> S;
+    static_for<0, RB>([&](auto rb) {
         static_for<0, X::NDT>([&](auto t) { S.o[rb][t] = f32x4_t{0.f, 0.f, 0.f, 0.f}; });
         S.m[rb] = -INFINITY;
         S.lsum[rb] = 0.f;
     });
-    wide_stream<D>(L, qb, a.qk_scale, lds, S);
+    wide_stream<D, RB, fused_prompt_depth<D>()>(L, qb, a.qk_scale, lds, S);
 
-    char *part = reinterpret_cast<char *>(a.part);
-    static_for<0, X::RB>([&](auto rb) {
+    const __amdgpu_buffer_rsrc_t r = part_rsrc(a);
+    static_for<0, RB>([&](auto rb) {
         float l = S.lsum[rb];
         l += __shfl_xor(l, 16);
         l += __shfl_xor(l, 32);
         if (ok[rb]) {
-            char *slot = part + slot_off(a, cell[rb], g, pk);
+            const uint32_t slot = slot_off(a, cell[rb], g, pk);
             static_for<0, X::NDT>([&](auto t) {
-                *reinterpret_cast<f32x4_t *>(slot + (size_t)(hh[rb] * D + 16 * t + 4 * quad) * 4) = S.o[rb][t];
+                part_store4(r, slot + (uint32_t)(hh[rb] * D + 16 * t + 4 * quad) * 4u, S.o[rb][t]);
             });
             if (quad == 0) {
-                *reinterpret_cast<float *>(slot + (size_t)(G * D + hh[rb]) * 4) = S.m[rb];
-                *reinterpret_cast<float *>(slot + (size_t)(G * D + G + hh[rb]) * 4) = l;
+                part_store1(r, slot + (uint32_t)(G * D + hh[rb]) * 4u, S.m[rb]);
+                part_store1(r, slot + (uint32_t)(G * D + G + hh[rb]) * 4u, l);
             }
         }
     });
+    stores_performed();
+    // count this chunk on each cell of the group
+    const int c0 = first_cell + grp * (X::ROWS / G);
+    const int n_cells = min(X::ROWS / G, end_cell - c0);
+    if ((int)threadIdx.x < n_cells) {
+        const int c = a.order[c0 + threadIdx.x];
+        if (arrive(a, c, g)) s_list[1 + atomicAdd(&s_list[0], 1)] = c;
+    }
+    __syncthreads();
+    return g;
 }
 
-// Launch 2: one work group per (cell, KV head) streams the cell's generated
-// rows (four waves, interleaved tiles), merges its waves,
-// folds in the prompt partials of launch 1 in chunk order and then the ZERO
-// term (n_zero keys of score 0 and value 0), and writes out and lse.
+// Generated-row item.  After streaming, thread 0 polls the (cell, KV head)
+// counter until every prompt chunk has stored its partial (at most
+// a.wait_polls polls; prompt items have lower block indices and never wait,
+// so they are dispatched first and finish).  Then this item merges in place:
+// its own partial is the last slot and never leaves the chip.  Past the
+// bound it stores its partial and counts itself like any other item, and the
+// last arrival merges.
 template <int D, int G>
-__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(waves_per_simd(D, kGenDepth))))
-void gen_merge_kernel(AttnArgs a) {
+__device__ int fused_gen_item(const AttnArgs &a, int item, char *lds, int *s_list) {
     using W = WaveMfma<D>;
-    __shared__ __attribute__((aligned(16))) char buf[CellwiseLds<D, G>::BYTES];
-    const int g = blockIdx.x % a.Hkv;
-    const int c = blockIdx.x / a.Hkv;
+    const int g = item % a.Hkv;
+    const int c = item / a.Hkv;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int col = threadIdx.x & 15;
     bf16x8_t qb[W::NDS];
@@ -622,42 +672,95 @@ void gen_merge_kernel(AttnArgs a) {
     WaveState<D> S;
     state_init(S);
     const ColMask cm{true, true, true};
-    wave_stream<D, kGenDepth, kGenAux>(L, wave, kWaves, cm, qb, a.qk_scale, buf + wave * W::LDS, S);
+    wave_stream<D, fused_gen_depth<D>(), kGenAux>(L, wave, kWaves, cm, qb, a.qk_scale, lds + wave * W::LDS, S);
     state_finish(S);
 
-    const bool zero_term = a.zero_donor && bit_set(a.spliced, c) && a.sb > a.sa;
-    const char *part = reinterpret_cast<const char *>(a.part);
-    const size_t base = slot_off(a, c, g, 0);
-    const size_t slot_bytes = (size_t)a.slot_floats * 4;
-    waves_merge<D, G>(S, buf, [&](int h, int d, float M, float Lsum, f32x4_t O) {
-        auto fold = [&](float mk, float lk, f32x4_t ok) __attribute__((always_inline)) {
-            const float mn = fmaxf(M, mk);
-            const float ms = mn == -INFINITY ? 0.f : mn;
-            const float fo = fast_exp2(M - ms), fn = fast_exp2(mk - ms);
-            Lsum = Lsum * fo + lk * fn;
-            O = O * fo + ok * fn;
-            M = mn;
-        };
-        constexpr int B = 8;
-        for (int k0 = 0; k0 < a.n_slots; k0 += B) {
-            f32x4_t ok[B];
-            float mk[B], lk[B];
-#pragma unroll
-            for (int j = 0; j < B; ++j) {
-                const char *sb = part + base + (size_t)min(k0 + j, a.n_slots - 1) * slot_bytes;
-                ok[j] = *reinterpret_cast<const f32x4_t *>(sb + (size_t)(h * D + d) * 4);
-                mk[j] = *reinterpret_cast<const float *>(sb + (size_t)(G * D + h) * 4);
-                lk[j] = *reinterpret_cast<const float *>(sb + (size_t)(G * D + G + h) * 4);
-            }
-#pragma unroll
-            for (int j = 0; j < B; ++j)
-                if (k0 + j < a.n_slots) fold(mk[j], lk[j], ok[j]);
+    int *cnt = a.counters + c * a.Hkv + g;
+    if (threadIdx.x == 0) {
+        bool ready = a.n_p == 0;
+        for (int i = 0; !ready && i < a.wait_polls; ++i) {
+            ready = __hip_atomic_load(cnt, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) >= a.n_p;
+            if (!ready) __builtin_amdgcn_s_sleep(4);
         }
-        if (zero_term) fold(0.f, (float)(a.sb - a.sa), f32x4_t{0.f, 0.f, 0.f, 0.f});
-        const int row = c * a.Hq + g * G + h;
-        *reinterpret_cast<f32x4_t *>(a.out + (size_t)row * D + d) = O * (1.f / Lsum);
-        if (d == 0) a.lse[row] = (M + log2f(Lsum)) * kLn2;
-    });
+        s_list[0] = ready ? -1 : 0;
+    }
+    __syncthreads();   // also: every wave is done with its V^T tile
+    const bool ready = s_list[0] < 0;
+    const __amdgpu_buffer_rsrc_t r = part_rsrc(a);
+    const uint32_t base = slot_off(a, c, g, 0);
+    const uint32_t slot_bytes = (uint32_t)a.slot_floats * 4u;
+    if (ready) {
+        // stage the prompt slots' (m, l) behind the wave-merge buffer
+        float *s_pm = reinterpret_cast<float *>(lds + FusedLds<D, G>::WAVE_MERGE);
+        float *s_pl = s_pm + kMaxSlots * G;
+        for (int t = threadIdx.x; t < a.n_p * G; t += kThreads) {
+            const uint32_t off = base + (uint32_t)(t / G) * slot_bytes;
+            s_pm[t] = part_load1(r, off + (uint32_t)(G * D + t % G) * 4u);
+            s_pl[t] = part_load1(r, off + (uint32_t)(G * D + G + t % G) * 4u);
+        }
+        const bool zero_term = has_zero_term(a, c);
+        waves_merge<D, G>(S, lds, [&](int h, int d, float Mg, float Lg, f32x4_t Og) {
+            float M = zero_term ? 0.f : -INFINITY;
+            for (int k = 0; k < a.n_p; ++k) M = fmaxf(M, s_pm[k * G + h]);
+            M = fmaxf(M, Mg);
+            float Ls = zero_term ? (float)(a.sb - a.sa) * fast_exp2(-M) : 0.f;
+            f32x4_t O = {0.f, 0.f, 0.f, 0.f};
+            constexpr int B = 8;
+            for (int k0 = 0; k0 < a.n_p; k0 += B) {
+                f32x4_t ok[B];
+#pragma unroll
+                for (int j = 0; j < B; ++j)
+                    ok[j] = part_load4(r, base + (uint32_t)min(k0 + j, a.n_p - 1) * slot_bytes +
+                                              (uint32_t)(h * D + d) * 4u);
+#pragma unroll
+                for (int j = 0; j < B; ++j)
+                    if (k0 + j < a.n_p) fold_slot(s_pm[(k0 + j) * G + h], s_pl[(k0 + j) * G + h], ok[j], M, Ls, O);
+            }
+            fold_slot(Mg, Lg, Og, M, Ls, O);   // this item's slot, a.n_p, comes last
+            write_row(a, c * a.Hq + g * G + h, d, D, M, Ls, O);
+        });
+        if (threadIdx.x == 0) {
+            __hip_atomic_store(cnt, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            s_list[0] = 0;   // nothing left to merge
+        }
+    } else {
+        const uint32_t slot = slot_off(a, c, g, a.n_p);
+        waves_merge<D, G>(S, lds, [&](int h, int d, float M, float Lsum, f32x4_t O) {
+            part_store4(r, slot + (uint32_t)(h * D + d) * 4u, O);
+            if (d == 0) {
+                part_store1(r, slot + (uint32_t)(G * D + h) * 4u, M);
+                part_store1(r, slot + (uint32_t)(G * D + G + h) * 4u, Lsum);
+            }
+        });
+        stores_performed();
+        if (threadIdx.x == 0 && arrive(a, c, g)) {
+            s_list[0] = 1;
+            s_list[1] = c;
+        }
+    }
+    __syncthreads();
+    return g;
+}
+
+template <int D, int G>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(fused_waves_per_simd(D))))
+void fused_kernel(AttnArgs a) {
+    __shared__ __attribute__((aligned(16))) char lds[FusedLds<D, G>::BYTES];
+    constexpr int MAXM = fused_max_merge<D, G>();
+    __shared__ int s_list[1 + MAXM];   // [0] count, [1..] cells to merge
+    static_assert(MAXM <= kThreads, "one thread per cell of a row group");
+    if (threadIdx.x == 0) s_list[0] = 0;
+    __syncthreads();
+    const int g = (int)blockIdx.x < a.n_prompt_items
+                      ? fused_prompt_item<D, G>(a, blockIdx.x, lds, s_list)
+                      : fused_gen_item<D, G>(a, blockIdx.x - a.n_prompt_items, lds, s_list);
+    const int n = s_list[0];
+    // merge in batches whose (m, l) staging fits
+    const int per = max(1, (kRowBlock * kMaxSlots) / (a.n_slots * G));
+    for (int i = 0; i < n; i += per) {
+        combine_cells<D, G>(a, s_list + 1 + i, min(per, n - i), g, lds);
+        __syncthreads();
+    }
 }
 
 // ------------------------------------------------------- cellwise kernel
@@ -717,75 +820,20 @@ __global__ __launch_bounds__(kThreads) void cellwise_kernel(AttnArgs a) {
     });
 }
 
-// bf16 cellwise kernel: the same per-(cell, KV head) work group, streaming
-// the cell's list on the matrix cores.  The list is cut into segments that
-// are contiguous in memory -- prompt before the span, the span (clean or
-// donor; absent for a ZERO splice), prompt after the span, generated rows --
-// and the span segment exists whether or not the cell is spliced, so a
-// splice never moves a tile boundary.
-template <int D, int G>
-__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(waves_per_simd(D, cellwise_depth(D)))))
-void cellwise_mfma_kernel(AttnArgs a) {
-    using W = WaveMfma<D>;
-    __shared__ __attribute__((aligned(16))) char buf[CellwiseLds<D, G>::BYTES];
-    const int g = blockIdx.x % a.Hkv;
-    const int c = blockIdx.x / a.Hkv;
-    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);   // uniform: tile pointers stay scalar
-    const int col = threadIdx.x & 15;
-    bf16x8_t qb[W::NDS];
-    load_q_cols<D>(a.q + ((size_t)c * a.Hq + (size_t)g * G + col % G) * W::ROW, qb);
-    const bool spl = bit_set(a.spliced, c);
-    const bool zskip = spl && a.zero_donor;
-    const bool from_donor = spl && !a.zero_donor;
-    const size_t head = (size_t)g * a.Tp * W::ROW;
-    KeyList L;
-    list_init(L);
-    if (a.Tp > 0) {
-        list_add(L, a.ck + head + (size_t)a.jp0 * W::ROW, a.cv + head + (size_t)a.jp0 * W::ROW, a.sa - a.jp0);
-        if (!zskip)
-            list_add(L, pick_base(from_donor, a.ck, a.dk) + head + (size_t)a.sa * W::ROW,
-                     pick_base(from_donor, a.cv, a.dv) + head + (size_t)a.sa * W::ROW, a.sb - a.sa);
-        list_add(L, a.ck + head + (size_t)a.sb * W::ROW, a.cv + head + (size_t)a.sb * W::ROW, a.Tp - a.sb);
-    }
-    const size_t goff = (((size_t)c * a.Hkv + g) * (size_t)a.cap + a.i0) * W::ROW;
-    list_add(L, a.gk + goff, a.gv + goff, a.n_gen);
-    WaveState<D> S;
-    state_init(S);
-    const ColMask cm{true, true, true};
-    wave_stream<D, cellwise_depth(D), kCellwiseAux>(L, wave, kWaves, cm, qb, a.qk_scale, buf + wave * W::LDS, S);
-    state_finish(S);
-    const int nsv = a.sb - a.sa;
-    const bool zero_term = zskip && nsv > 0;
-    waves_merge<D, G>(S, buf, [&](int h, int d, float M, float L, f32x4_t O) {
-        if (zero_term) {   // nsv keys of score 0 and value 0
-            const float Mz = fmaxf(M, 0.f);
-            const float f = fast_exp2(M - Mz);
-            L = L * f + (float)nsv * fast_exp2(-Mz);
-            O *= f;
-            M = Mz;
-        }
-        const int row = c * a.Hq + g * G + h;
-        *reinterpret_cast<f32x4_t *>(a.out + (size_t)row * D + d) = O * (1.f / L);
-        if (d == 0) a.lse[row] = (M + log2f(L)) * kLn2;
-    });
-}
-
 // ------------------------------------------------------------ dispatch
 
 typedef void (*attn_fn)(AttnArgs);
 struct AttnKernels {
-    attn_fn items;      // f32: one launch of prompt and generated items
-    attn_fn cellwise;   // short prompts: one work group per (cell, KV head)
-    attn_fn prompt;     // bf16 launch 1: shared-prompt contraction
-    attn_fn gen;        // bf16 launch 2: generated rows and the merge
+    attn_fn items;      // one launch of prompt and generated-row items with merge
+    attn_fn cellwise;   // f32, short prompts: one work group per (cell, KV head)
 };
 
 template <int D, int G, bool BF16>
 AttnKernels kernels_of() {
     if constexpr (BF16)
-        return AttnKernels{nullptr, cellwise_mfma_kernel<D, G>, prompt_wide_kernel<D, G>, gen_merge_kernel<D, G>};
+        return AttnKernels{fused_kernel<D, G>, nullptr};
     else
-        return AttnKernels{items_kernel<D, G>, cellwise_kernel<D, G, BF16>, nullptr, nullptr};
+        return AttnKernels{items_kernel<D, G>, cellwise_kernel<D, G, BF16>};
 }
 
 template <int D, bool BF16>
@@ -795,7 +843,7 @@ AttnKernels pick_g(int G) {
     case 2: return kernels_of<D, 2, BF16>();
     case 4: return kernels_of<D, 4, BF16>();
     case 8: return kernels_of<D, 8, BF16>();
-    default: return AttnKernels{nullptr, nullptr, nullptr, nullptr};
+    default: return AttnKernels{nullptr, nullptr};
     }
 }
 

@@ -99,19 +99,19 @@ inline bool cell_spliced(const int32_t *cell_LW, int c, int layer, int step) {
 
 // ---------------------------------------------------------------- attention plan
 //
-// bf16 inputs:
-//   cellwise (prompt of at most kCellwiseMaxPrompt visible keys): one launch,
-//     one work group per (cell, KV head) streaming the cell's whole list;
-//   otherwise two launches:
-//     1. prompt kernel: work groups (KV head, group of wide_rows(D) rows,
-//        prompt chunk); the rows of a KV head are the (cell, q head) pairs of
-//        every cell, clean cells first, and each K/V tile is staged in LDS
-//        once for all of them; every row gets one partial result per chunk;
-//     2. generated-row kernel: one work group per (cell, KV head) streams the
-//        cell's generated rows and folds in its prompt partials.
-// f32 inputs (vector ALUs, one launch): prompt items (cell, KV head, prompt
-//   chunk) and generated items (cell, KV head, generated chunk); the last item
-//   of a (cell, KV head) to finish merges its partials.
+// bf16 inputs: one launch of two kinds of items:
+//     prompt items: work groups (KV head, group of group_rows(D) rows, prompt
+//       chunk); the rows of a KV head are the (cell, q head) pairs of every
+//       cell, clean cells first, and each K/V tile is staged in LDS once for
+//       all of a group's rows; every row gets one partial result per chunk;
+//     generated-row items: one work group per (cell, KV head) streams the
+//       cell's generated rows into one more partial result;
+//   the last item of a (cell, KV head) to finish merges its partials.
+// f32 inputs (vector ALUs, one launch): prompts of at most
+//   kCellwiseMaxPrompt visible keys take one work group per (cell, KV head)
+//   streaming the cell's whole list; longer ones prompt items (cell, KV head,
+//   prompt chunk) and generated items (cell, KV head, generated chunk),
+//   merged the same way.
 
 constexpr int kRowBlock = 64;              // rows of the f32 merge staging
 constexpr int kMinChunk = 256;             // a default chunk is at least this long
@@ -122,11 +122,15 @@ constexpr int kGenItemsTarget = 2048;      // f32 generated items a default spli
 constexpr int kWideItemsTarget = 512;      // bf16 prompt work groups a default split aims for
 constexpr int kWideMinChunk = 128;         // a default bf16 prompt chunk is at least this long
 
-// bf16 prompt kernel: 16-row MFMA blocks per wave (so that a wave's output
-// accumulators, RB * D / 4 registers, stay at 64) and rows per work group
-// (four waves).
-constexpr int wide_row_blocks(int D) { return 256 / D; }
-constexpr int wide_rows(int D) { return 4 * 16 * wide_row_blocks(D); }
+// bf16 prompt items: 16-row MFMA blocks per wave (a wave's output
+// accumulators, RB * D / 4 registers, stay at 32 for D <= 128) and rows per
+// work group (four waves).
+constexpr int fused_row_blocks(int D) { return D <= 64 ? 2 : 1; }
+constexpr int group_rows(int D) { return 4 * 16 * fused_row_blocks(D); }
+
+// Work groups are handed to the GPU's eight XCDs in turn (block b to XCD
+// b mod 8); the bf16 prompt grid is laid out in rounds of this many blocks.
+constexpr int kXcds = 8;
 
 inline int ceil_div(int64_t a, int64_t b) { return (int)((a + b - 1) / b); }
 inline int round_up(int64_t a, int64_t m) { return (int)((a + m - 1) / m * m); }
@@ -137,15 +141,15 @@ inline int slot_floats(int G, int D) { return (G * D + 2 * G + 63) / 64 * 64; }
 inline bool bf16_path(const splice_shape &sh) { return sh.dtype == SPLICE_BF16; }
 
 // bf16 row groups of one KV head: the rows of unspliced cells and the rows
-// of spliced cells are grouped separately (wide_rows(D) rows per group), so
+// of spliced cells are grouped separately (group_rows(D) rows per group), so
 // no group needs both the clean and the donor span.  n_clean cells of C are
 // unspliced at the call.
 inline int clean_row_groups(const splice_shape &sh, int n_clean) {
-    return ceil_div((int64_t)n_clean * group_of(sh), wide_rows(sh.head_dim));
+    return ceil_div((int64_t)n_clean * group_of(sh), group_rows(sh.head_dim));
 }
 inline int row_groups(const splice_shape &sh, int n_clean) {
     return clean_row_groups(sh, n_clean) +
-           ceil_div((int64_t)(sh.n_cells - n_clean) * group_of(sh), wide_rows(sh.head_dim));
+           ceil_div((int64_t)(sh.n_cells - n_clean) * group_of(sh), group_rows(sh.head_dim));
 }
 
 // Prompt work groups per prompt chunk.  The bf16 count depends on the call's
@@ -156,7 +160,7 @@ inline int prompt_items_per_chunk(const splice_shape &sh, int n_clean) {
 }
 inline int prompt_items_bound(const splice_shape &sh) {
     if (!bf16_path(sh)) return sh.n_kv_heads * sh.n_cells;
-    return sh.n_kv_heads * (ceil_div((int64_t)sh.n_cells * group_of(sh), wide_rows(sh.head_dim)) + 1);
+    return sh.n_kv_heads * (ceil_div((int64_t)sh.n_cells * group_of(sh), group_rows(sh.head_dim)) + 1);
 }
 
 inline int prompt_chunk_target(const splice_shape &sh) {
@@ -167,7 +171,7 @@ inline int prompt_chunk_target(const splice_shape &sh) {
 }
 
 inline int gen_chunk_target(const splice_shape &sh) {
-    if (bf16_path(sh)) return 1;   // one generated-row work group per (cell, KV head)
+    if (bf16_path(sh)) return 1;   // one generated-row item per (cell, KV head)
     const int64_t pairs = (int64_t)sh.n_cells * sh.n_kv_heads;
     const int64_t t = pairs > 0 ? kGenItemsTarget / pairs : 1;
     return t < 1 ? 1 : (t > kMaxChunks ? kMaxChunks : (int)t);
@@ -192,9 +196,9 @@ inline void cut(int n, int target, int split, int *k, int *len, int min_chunk = 
     *k = ceil_div(n, *len);
 }
 
-// Prompts up to this many visible keys take the cellwise path: each (cell,
-// KV head) streams its own list, re-reading the shared prompt from L2,
-// which costs less than the row-block path's split and merge.
+// f32 prompts up to this many visible keys take the cellwise path: each
+// (cell, KV head) streams its own list, re-reading the shared prompt from L2,
+// which costs less than the split and merge of the item path.
 constexpr int kCellwiseMaxPrompt = 512;
 
 struct AttnPlan {
@@ -216,7 +220,7 @@ inline int count_clean(const splice_shape &sh, const splice_call &call, const in
 inline AttnPlan plan_attn(const splice_shape &sh, const splice_call &call, int n_clean) {
     AttnPlan p;
     p.geo = geometry(sh, call);
-    p.cellwise = call.split_keys == 0 && p.geo.n_prompt <= kCellwiseMaxPrompt;
+    p.cellwise = !bf16_path(sh) && call.split_keys == 0 && p.geo.n_prompt <= kCellwiseMaxPrompt;
     if (p.cellwise) {
         p.n_p = p.n_g = 0;
         p.p_len = p.g_len = 64;
@@ -227,15 +231,19 @@ inline AttnPlan plan_attn(const splice_shape &sh, const splice_call &call, int n
     cut(p.geo.n_prompt, prompt_chunk_target(sh), call.split_keys, &p.n_p, &p.p_len,
         bf16_path(sh) ? kWideMinChunk : kMinChunk);
     if (bf16_path(sh)) {
-        // the generated-row work group folds the prompt partials in itself
+        // one generated-row item per (cell, KV head), its four waves merged
         p.n_g = 1;
         p.g_len = p.geo.n_gen;
-        p.n_slots = p.n_p;
     } else {
         cut(p.geo.n_gen, gen_chunk_target(sh), call.split_keys, &p.n_g, &p.g_len);
-        p.n_slots = p.n_p + p.n_g;
     }
-    p.n_prompt_items = prompt_items_per_chunk(sh, n_clean) * p.n_p;
+    p.n_slots = p.n_p + p.n_g;
+    if (bf16_path(sh)) {
+        // units (KV head, chunk) padded to whole rounds of kXcds, times row groups
+        p.n_prompt_items = kXcds * row_groups(sh, n_clean) * ceil_div((int64_t)sh.n_kv_heads * p.n_p, kXcds);
+    } else {
+        p.n_prompt_items = prompt_items_per_chunk(sh, n_clean) * p.n_p;
+    }
     p.n_gen_items = sh.n_cells * sh.n_kv_heads * p.n_g;
     return p;
 }
@@ -272,7 +280,7 @@ inline int max_default_chunks(int n, int target, int min_chunk = kMinChunk) {
 inline int worst_default_slots(const splice_shape &sh) {
     const int prompt = max_default_chunks(sh.prompt_len, prompt_chunk_target(sh),
                                           bf16_path(sh) ? kWideMinChunk : kMinChunk);
-    return bf16_path(sh) ? prompt : prompt + max_default_chunks(sh.gen_capacity, gen_chunk_target(sh));
+    return bf16_path(sh) ? prompt + 1 : prompt + max_default_chunks(sh.gen_capacity, gen_chunk_target(sh));
 }
 
 }  // namespace splice

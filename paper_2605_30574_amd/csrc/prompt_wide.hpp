@@ -8,7 +8,8 @@
 //                 multiplied into all RB row blocks (v_mfma_f32_16x16x32_bf16);
 //   online softmax per row (column of S), masked per segment class;
 //   O^T += V^T P: each 16 d x 32 keys V^T operand is read once and multiplied
-//                 into all RB row blocks, P split into bf16 high and remainder.
+//                 into all RB row blocks, P rounded to bf16 (the sums of P
+//                 stay in fp32).
 // The LDS tiles are double-buffered and the global loads of the next
 // DEPTH - 1 tiles are in flight while one is computed; one barrier per tile
 // orders the buffers.
@@ -19,10 +20,10 @@
 
 namespace splice_dev {
 
-template <int D>
+template <int D, int RB_>
 struct Wide {
-    static constexpr int RB = splice::wide_row_blocks(D);   // 16-row blocks per wave
-    static constexpr int ROWS = splice::wide_rows(D);       // rows per work group
+    static constexpr int RB = RB_;                          // 16-row blocks per wave
+    static constexpr int ROWS = 4 * 16 * RB;                // rows per work group
     static constexpr int TK = 32;                           // keys per tile
     static constexpr int ROW = D * 2;                       // bytes per K or V row
     static constexpr int NDS = D / 32;                      // k-steps of q.k
@@ -33,20 +34,23 @@ struct Wide {
     static constexpr int BUF = KTILE + D * VROW;            // one staged tile
     static constexpr int LDS = 2 * BUF;                     // double buffer
     static constexpr int NKU = TK * (D / 8) / kThreads;     // 16-byte K units per thread
-    static constexpr int VU = (D / 8) * (TK / 4);           // V units (4 keys x 8 d): thread tid < VU owns one
-    static_assert(NKU >= 1 && VU <= kThreads, "tile staging assumes 64 <= D <= 256");
+    static constexpr int VU = (D / 8) * (TK / 2);           // V units: 2 keys x 8 d
+    static constexpr int NVU = (VU + kThreads - 1) / kThreads;   // V units per thread
+    static_assert(NKU >= 1 && NVU <= 2, "tile staging assumes 64 <= D <= 256");
 };
 
 // One thread's share of a tile in flight.
 template <int D>
 struct WideRegs {
-    u32x4_t k[Wide<D>::NKU];
-    u32x4_t v[4];
+    u32x4_t k[Wide<D, 1>::NKU];
+    u32x4_t v[Wide<D, 1>::NVU][2];
 };
 
+// K: unit u is 16 bytes of key row u / (D / 8).  V: unit u holds keys
+// 2 kp, 2 kp + 1 (kp = u mod 16) at bytes 16 dg .. 16 dg + 15 (dg = u / 16).
 template <int D>
 __device__ __forceinline__ void wide_fetch(const TileRef &t, WideRegs<D> &r) {
-    using X = Wide<D>;
+    using X = Wide<D, 1>;
     const int tid = threadIdx.x;
     const __amdgpu_buffer_rsrc_t rk = rows_rsrc(t.k, t.n * X::ROW);
     const __amdgpu_buffer_rsrc_t rv = rows_rsrc(t.v, t.n * X::ROW);
@@ -54,17 +58,22 @@ __device__ __forceinline__ void wide_fetch(const TileRef &t, WideRegs<D> &r) {
         const int u = tid + kThreads * i;
         r.k[i] = row_load<0>(rk, (u / (D / 8)) * X::ROW + (u % (D / 8)) * 16);
     });
-    if (tid < X::VU) {
-        const int kq = tid & 7, dg = tid >> 3;   // keys 4 kq .. 4 kq + 3, bytes 16 dg ..
-        static_for<0, 4>([&](auto kk) { r.v[kk] = row_load<0>(rv, (4 * kq + kk) * X::ROW + 16 * dg); });
-    }
+    static_for<0, X::NVU>([&](auto i) {
+        const int u = tid + kThreads * i;
+        if (X::VU % kThreads == 0 || u < X::VU) {
+            const int kp = u & 15, dg = u >> 4;
+            r.v[i][0] = row_load<0>(rv, (2 * kp) * X::ROW + 16 * dg);
+            r.v[i][1] = row_load<0>(rv, (2 * kp + 1) * X::ROW + 16 * dg);
+        }
+    });
 }
 
 // K row-major (16-byte units), V transposed: row d holds the tile's keys.
-// Eight lanes of consecutive kq fill one 64-byte V^T row segment.
+// The 16 lanes of one dg fill a 64-byte V^T row segment; the four dg of a
+// wave land 8 rows apart, 16 banks apart.
 template <int D>
 __device__ __forceinline__ void wide_stage(const WideRegs<D> &r, char *buf) {
-    using X = Wide<D>;
+    using X = Wide<D, 1>;
     const int tid = threadIdx.x;
     char *sK = buf;
     char *sV = buf + X::KTILE;
@@ -72,36 +81,38 @@ __device__ __forceinline__ void wide_stage(const WideRegs<D> &r, char *buf) {
         const int u = tid + kThreads * i;
         *reinterpret_cast<u32x4_t *>(sK + (u / (D / 8)) * X::KROW + (u % (D / 8)) * 16) = r.k[i];
     });
-    if (tid < X::VU) {
-        const int kq = tid & 7, dg = tid >> 3;
-        static_for<0, 8>([&](auto j) {
-            constexpr int jj = decltype(j)::value;
-            constexpr uint32_t sel = (jj & 1) ? 0x07060302u : 0x05040100u;
-            const uint32_t lo = __builtin_amdgcn_perm(r.v[1][jj >> 1], r.v[0][jj >> 1], sel);
-            const uint32_t hi = __builtin_amdgcn_perm(r.v[3][jj >> 1], r.v[2][jj >> 1], sel);
-            *reinterpret_cast<u32x2_t *>(sV + (8 * dg + jj) * X::VROW + 8 * kq) = u32x2_t{lo, hi};
-        });
-    }
+    static_for<0, X::NVU>([&](auto i) {
+        const int u = tid + kThreads * i;
+        if (X::VU % kThreads == 0 || u < X::VU) {
+            const int kp = u & 15, dg = u >> 4;
+            static_for<0, 8>([&](auto j) {
+                constexpr int jj = decltype(j)::value;
+                constexpr uint32_t sel = (jj & 1) ? 0x07060302u : 0x05040100u;
+                *reinterpret_cast<uint32_t *>(sV + (8 * dg + jj) * X::VROW + 4 * kp) =
+                    __builtin_amdgcn_perm(r.v[i][1][jj >> 1], r.v[i][0][jj >> 1], sel);
+            });
+        }
+    });
 }
 
 // Streaming state of one wave: RB row blocks, lane (quad, col) holding row
 // block rb's column col (o[rb][t][i] = O^T[16 t + 4 quad + i][col]).
-template <int D>
+template <int D, int RB>
 struct WideState {
-    f32x4_t o[Wide<D>::RB][Wide<D>::NDT];
-    float m[Wide<D>::RB];
-    float lsum[Wide<D>::RB];
+    f32x4_t o[RB][Wide<D, RB>::NDT];
+    float m[RB];
+    float lsum[RB];
 };
 
 // One staged tile for this wave's RB row blocks.  A work group's rows all
 // belong to one class (unspliced or spliced cells), so every tile of its list
 // is visible to every row; rows past the last cell compute values that are
 // never stored.  Only a partial tile (n_valid < TK) masks keys.
-template <int D>
+template <int D, int RB>
 __device__ __forceinline__ void wide_compute(const char *buf, int n_valid,
-                                             const bf16x8_t (&qb)[Wide<D>::RB][Wide<D>::NDS], float qk_scale,
-                                             WideState<D> &S) {
-    using X = Wide<D>;
+                                             const bf16x8_t (&qb)[RB][Wide<D, RB>::NDS], float qk_scale,
+                                             WideState<D, RB> &S) {
+    using X = Wide<D, RB>;
     const int lane = threadIdx.x & 63, col = lane & 15, quad = lane >> 4;
     const char *sK = buf;
     const char *sV = buf + X::KTILE;
@@ -119,7 +130,7 @@ __device__ __forceinline__ void wide_compute(const char *buf, int n_valid,
             });
         });
     });
-    bf16x8_t ph[X::RB], pl[X::RB];
+    bf16x8_t pb[X::RB];
     static_for<0, X::RB>([&](auto rb) {
         float x[2][4];
         static_for<0, 2>([&](auto h) {
@@ -149,9 +160,7 @@ __device__ __forceinline__ void wide_compute(const char *buf, int n_valid,
             constexpr int jj = decltype(j)::value;
             const float p = fast_exp2(x[jj >> 2][jj & 3] - ms);
             S.lsum[rb] += p;
-            const __bf16 hb = (__bf16)p;
-            ph[rb][jj] = hb;
-            pl[rb][jj] = (__bf16)(p - (float)hb);
+            pb[rb][jj] = (__bf16)p;
         });
     });
     // k-slot 8 quad + j is key 4 quad + j (j < 4) or 16 + 4 quad + (j - 4):
@@ -162,8 +171,7 @@ __device__ __forceinline__ void wide_compute(const char *buf, int n_valid,
         const uint2 vb = *reinterpret_cast<const uint2 *>(vrow + 32 + 8 * quad);
         const bf16x8_t vf = __builtin_bit_cast(bf16x8_t, make_uint4(va.x, va.y, vb.x, vb.y));
         static_for<0, X::RB>([&](auto rb) {
-            S.o[rb][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, ph[rb], S.o[rb][t], 0, 0, 0);
-            S.o[rb][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pl[rb], S.o[rb][t], 0, 0, 0);
+            S.o[rb][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pb[rb], S.o[rb][t], 0, 0, 0);
         });
     });
 }
@@ -179,11 +187,10 @@ constexpr int wide_depth() { return D <= 128 ? 3 : 2; }
 // orders the buffers.  The loop is unrolled DEPTH times so that the register
 // sets are only ever indexed by constants.  Called by all threads of the
 // work group.
-template <int D>
-__device__ __forceinline__ void wide_stream(const KeyList &L, const bf16x8_t (&qb)[Wide<D>::RB][Wide<D>::NDS],
-                                            float qk_scale, char *lds, WideState<D> &S) {
-    using X = Wide<D>;
-    constexpr int DEPTH = wide_depth<D>();
+template <int D, int RB, int DEPTH>
+__device__ __forceinline__ void wide_stream(const KeyList &L, const bf16x8_t (&qb)[RB][Wide<D, RB>::NDS],
+                                            float qk_scale, char *lds, WideState<D, RB> &S) {
+    using X = Wide<D, RB>;
     const int n_tiles = list_tiles(L);
     if (n_tiles == 0) return;
     WideRegs<D> r[DEPTH];
@@ -206,7 +213,7 @@ __device__ __forceinline__ void wide_stream(const KeyList &L, const bf16x8_t (&q
             ref[j] = list_tile_or_empty<X::TK>(L, t + DEPTH, n_tiles, X::ROW);
             wide_fetch<D>(ref[j], r[j]);
             if (live) {
-                wide_compute<D>(lds + (t & 1) * X::BUF, cur.n, qb, qk_scale, S);
+                wide_compute<D, RB>(lds + (t & 1) * X::BUF, cur.n, qb, qk_scale, S);
                 if (t + 1 < n_tiles) wide_stage<D>(r[jn], lds + ((t + 1) & 1) * X::BUF);
                 __syncthreads();   // the next buffer is staged; nobody reads this one any more
             }

@@ -114,7 +114,7 @@ AttnKernels pick_attn(int D, int G, int dtype) {
     case 64: return bf16 ? attn_kernels_d64_bf16(G) : attn_kernels_d64_f32(G);
     case 128: return bf16 ? attn_kernels_d128_bf16(G) : attn_kernels_d128_f32(G);
     case 256: return bf16 ? attn_kernels_d256_bf16(G) : attn_kernels_d256_f32(G);
-    default: return AttnKernels{nullptr, nullptr, nullptr, nullptr};
+    default: return AttnKernels{nullptr, nullptr};
     }
 }
 
@@ -258,7 +258,7 @@ int32_t splice_decode_attn(const splice_shape *shape, const splice_call *call, c
 
     const int G = splice::group_of(sh);
     const AttnKernels kern = pick_attn(sh.head_dim, G, sh.dtype);
-    if (!kern.cellwise) return SPLICE_EUNSUPPORTED;
+    if (!kern.items) return SPLICE_EUNSUPPORTED;
 
     const splice::Geometry &geo = plan.geo;
     AttnArgs a;
@@ -281,6 +281,7 @@ int32_t splice_decode_attn(const splice_shape *shape, const splice_call *call, c
     a.n_rb = splice::bf16_path(sh) ? splice::row_groups(sh, n_clean) : 0;
     a.n_rg_clean = splice::bf16_path(sh) ? splice::clean_row_groups(sh, n_clean) : 0;
     a.n_prompt_items = plan.n_prompt_items;
+    a.wait_polls = call->merge_wait == 0 ? kDefaultWaitPolls : (call->merge_wait < 0 ? 0 : call->merge_wait);
     a.qk_scale = call->scale * kLog2e;
     fill_mask(sh, *call, cell_LW, a.spliced);
     // row-block order: clean cells first, then spliced cells (each by index)
@@ -294,19 +295,6 @@ int32_t splice_decode_attn(const splice_shape *shape, const splice_call *call, c
 
     if (plan.cellwise) {
         hipLaunchKernelGGL(kern.cellwise, dim3((unsigned)(sh.n_cells * sh.n_kv_heads)), dim3(kThreads), 0,
-                           (hipStream_t)stream, a);
-        return launch_status();
-    }
-    if (sh.dtype == SPLICE_BF16) {
-        // launch 1 writes the prompt partials, launch 2 streams the generated
-        // rows and merges; stream order makes launch 1's stores visible
-        if (plan.n_prompt_items > 0) {
-            hipLaunchKernelGGL(kern.prompt, dim3((unsigned)plan.n_prompt_items), dim3(kThreads), 0,
-                               (hipStream_t)stream, a);
-            const int32_t st = launch_status();
-            if (st != SPLICE_OK) return st;
-        }
-        hipLaunchKernelGGL(kern.gen, dim3((unsigned)(sh.n_cells * sh.n_kv_heads)), dim3(kThreads), 0,
                            (hipStream_t)stream, a);
         return launch_status();
     }

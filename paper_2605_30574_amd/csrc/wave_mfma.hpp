@@ -7,9 +7,9 @@
 //               from memory straight into the operand layout; B = Q^T;
 //   online softmax per column (running maximum shared by the column's lanes);
 //   O^T += V^T P with v_mfma_f32_16x16x16_bf16: A = 16 d x 16 keys of V^T,
-//               read from a per-wave LDS tile that holds V transposed; B = P,
-//               which stays in the lanes where S came out, split into a bf16
-//               high part and a bf16 remainder (p carried to ~2^-17).
+//               read from a per-wave LDS tile that holds V transposed; B = P
+//               rounded to bf16, which stays in the lanes where S came out
+//               (the running sums of P stay in fp32).
 // The 16 columns are either the G heads of one (cell, KV head) repeated
 // (column j -> head j mod G), or 16 different (cell, head) rows of one KV
 // head reading a shared prompt.  Waves never synchronise with each other
@@ -268,21 +268,18 @@ __device__ __forceinline__ void tile_compute(const u32x4_t (&kr)[WaveMfma<D>::ND
         S.m = mn;
     }
     const float ms = S.m == -INFINITY ? 0.f : S.m;
-    i16x4_t ph, pl;
+    i16x4_t pb;
     static_for<0, 4>([&](auto i) {
         const float p = fast_exp2(x[i] - ms);
         S.lsum += p;
-        const __bf16 hb = (__bf16)p;
-        ph[(int)i] = __builtin_bit_cast(short, hb);
-        pl[(int)i] = __builtin_bit_cast(short, (__bf16)(p - (float)hb));
+        pb[(int)i] = __builtin_bit_cast(short, (__bf16)p);
     });
     // k-slot 4 quad + i of the p.v product is key 4 quad + i: the keys whose
     // scores this lane holds
     static_for<0, W::NDT>([&](auto t) {
         const uint2 va = *reinterpret_cast<const uint2 *>(sVt + (16 * t + col) * W::VROW + 8 * quad);
         const i16x4_t vf = __builtin_bit_cast(i16x4_t, va);
-        S.o[t] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(vf, ph, S.o[t], 0, 0, 0);
-        S.o[t] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(vf, pl, S.o[t], 0, 0, 0);
+        S.o[t] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(vf, pb, S.o[t], 0, 0, 0);
     });
 }
 

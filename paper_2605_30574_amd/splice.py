@@ -24,6 +24,7 @@ SPLICE_DONOR_BUFFER, SPLICE_DONOR_ZERO = 0, 1
 SPLICE_BF16, SPLICE_F32 = 0, 1
 SPLICE_SRC_CLEAN, SPLICE_SRC_DONOR, SPLICE_SRC_ZERO, SPLICE_SRC_GEN = 0, 1, 2, 3
 SPLICE_MAX_CELLS = 256
+SPLICE_ABI_VERSION = 2   # layout of SpliceShape / SpliceCall below
 
 EXPORTS = ("splice_abi_version", "splice_status_str", "splice_visible_len", "splice_kv_build",
            "splice_decode_attn_workspace_bytes", "splice_workspace_init", "splice_decode_attn")
@@ -37,7 +38,7 @@ class SpliceShape(ctypes.Structure):
 
 class SpliceCall(ctypes.Structure):
     _fields_ = [("layer", ctypes.c_int32), ("step", ctypes.c_int32), ("window", ctypes.c_int32),
-                ("scale", ctypes.c_float), ("split_keys", ctypes.c_int32)]
+                ("scale", ctypes.c_float), ("split_keys", ctypes.c_int32), ("merge_wait", ctypes.c_int32)]
 
 
 class SpliceError(RuntimeError):
@@ -76,6 +77,9 @@ def load_library(path: str = LIB_PATH):
     lib.splice_decode_attn.restype = i32
     lib.splice_decode_attn.argtypes = [shp, cal, i32p, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp,
                                        ctypes.c_size_t, vp]
+    got = lib.splice_abi_version()
+    if got != SPLICE_ABI_VERSION:
+        raise ImportError(f"{path} has ABI version {got}, this binding expects {SPLICE_ABI_VERSION}: rebuild it")
     _lib = lib
     return lib
 
@@ -104,8 +108,9 @@ def make_shape(n_cells: int, n_layers: int, n_q_heads: int, n_kv_heads: int, hea
                        SPLICE_BF16 if dtype == "bf16" else SPLICE_F32)
 
 
-def make_call(layer: int, step: int, window: int, scale: float, split_keys: int = 0) -> SpliceCall:
-    return SpliceCall(layer, step, window, float(scale), split_keys)
+def make_call(layer: int, step: int, window: int, scale: float, split_keys: int = 0,
+              merge_wait: int = 0) -> SpliceCall:
+    return SpliceCall(layer, step, window, float(scale), split_keys, merge_wait)
 
 
 def _cells(cell_LW, n_cells: int):

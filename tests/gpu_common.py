@@ -42,9 +42,9 @@ def host(bufs):
     return {k: workloads.to_numpy(v) for k, v in bufs.items()}
 
 
-def run_attn(w, layer, step, bufs, q, lw, split=0, ws=None, shape=None):
+def run_attn(w, layer, step, bufs, q, lw, split=0, ws=None, shape=None, merge_wait=0):
     shape = shape or shape_of(w, n_cells=q.shape[0])
-    call = sp.make_call(layer, step, w.window(layer), w.scale, split)
+    call = sp.make_call(layer, step, w.window(layer), w.scale, split, merge_wait)
     C = shape.n_cells
     out = torch.full((C, w.n_q_heads, w.head_dim), float("nan"), device="cuda", dtype=torch.float32)
     lse = torch.full((C, w.n_q_heads), float("nan"), device="cuda", dtype=torch.float32)

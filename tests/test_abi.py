@@ -25,7 +25,7 @@ def test_library_exports_every_declared_symbol():
     lib = sp.load_library()
     for name in declared:
         assert hasattr(lib, name), name
-    assert sp.splice_abi_version() == 1
+    assert sp.splice_abi_version() == 2
 
 
 def test_single_hip_runtime_mapped():

@@ -10,7 +10,7 @@ import gpu_common as gc
 import oracle_pins
 import paper_2605_30574_amd as sp
 import workloads
-from workloads import DONOR_BLANK
+from workloads import DONOR_BLANK, DONOR_ZERO
 
 pytestmark = pytest.mark.gpu
 
@@ -65,6 +65,29 @@ def test_batch_independence_and_determinism():
     pb = dict(bufs, gen_k=bufs["gen_k"][perm].contiguous(), gen_v=bufs["gen_v"][perm].contiguous())
     o_p, l_p = gc.run_attn(w, layer, step, pb, q[perm].contiguous(), lw[perm].copy(), split=128)
     assert np.array_equal(o_p, o_b[perm]) and np.array_equal(l_p, l_b[perm])
+
+
+@pytest.mark.parametrize("donor", [DONOR_BLANK, DONOR_ZERO])
+def test_merge_site_does_not_change_bits(donor):
+    """A generated-row item merges its (cell, KV head) in place after waiting
+    for the prompt partials, or -- past its polling bound -- leaves the merge
+    to the last item to finish.  Both follow one fold order, so the bits are
+    the same whichever item merged; merge_wait < 0 forces the hand-over on
+    every pair and 1 mixes the two within a call."""
+    w = _w().with_(donor=donor)
+    lw = workloads.cell_lw(w)
+    layer, step = 1, 150
+    bufs = gc.gpu_layer(w, layer)
+    hb = gc.host(bufs)
+    q = workloads.make_q(w, layer, step, device="cuda")
+    ref_o, ref_l = gc.run_oracle(w, layer, step, hb, workloads.to_numpy(q), lw)
+    gc.announce(f"merge site donor={donor}: in place")
+    o_w, l_w = gc.run_attn(w, layer, step, bufs, q, lw, split=64)
+    gc.assert_attn_close(o_w, l_w, ref_o, ref_l, "in place")
+    for mw in (-1, 1):
+        gc.announce(f"merge site donor={donor}: merge_wait={mw}")
+        o_h, l_h = gc.run_attn(w, layer, step, bufs, q, lw, split=64, merge_wait=mw)
+        assert np.array_equal(o_h, o_w) and np.array_equal(l_h, l_w), f"merge_wait={mw}"
 
 
 def test_split_changes_only_rounding():
