@@ -25,6 +25,7 @@ struct AttnArgs {
     int n_rb, n_prompt_items, n_clean;
     int n_rg_clean;   // bf16 prompt row groups of unspliced cells (the rest: spliced cells)
     int wait_polls;   // bf16 generated-row items: most polls for the prompt partials
+    int gen_pairs;    // bf16 generated-row items: (cell, KV head) pairs per work group
     float qk_scale;   // scale * log2(e)
     uint32_t spliced[SPLICE_MAX_CELLS / 32];
     uint8_t order[SPLICE_MAX_CELLS];   // clean cells, then spliced cells
@@ -396,13 +397,13 @@ __device__ __forceinline__ void write_row(const AttnArgs &a, int row, int d, int
 // groups of four consecutive outputs and loads them two slots at a time.
 constexpr int kMergeUnits = 4;
 
-template <int D, int G>
+template <int D, int G, int NT>
 __device__ void combine_cells(const AttnArgs &a, const int *list, int n, int g, char *buf) {
     const __amdgpu_buffer_rsrc_t r = part_rsrc(a);
     float *s_m = reinterpret_cast<float *>(buf);           // [n][n_slots][G]
     float *s_l = s_m + kRowBlock * kMaxSlots;               // [n][n_slots][G]
     const int per_cell = a.n_slots * G;
-    for (int t = threadIdx.x; t < n * per_cell; t += kThreads) {
+    for (int t = threadIdx.x; t < n * per_cell; t += NT) {
         const int i = t / per_cell, rem = t % per_cell;
         const int k = rem / G, h = rem % G;
         const uint32_t slot = slot_off(a, list[i], g, k);
@@ -413,14 +414,14 @@ __device__ void combine_cells(const AttnArgs &a, const int *list, int n, int g, 
     constexpr int UPC = G * D / 4;                           // 4-wide units per cell
     const int total = n * UPC;
     const uint32_t slot_bytes = (uint32_t)a.slot_floats * 4u;
-    for (int u0 = threadIdx.x; u0 < total; u0 += kThreads * kMergeUnits) {
+    for (int u0 = threadIdx.x; u0 < total; u0 += NT * kMergeUnits) {
         float M[kMergeUnits], L[kMergeUnits];
         f32x4_t O[kMergeUnits];
         uint32_t base[kMergeUnits];
         int sm_off[kMergeUnits];
 #pragma unroll
         for (int b = 0; b < kMergeUnits; ++b) {
-            const int u = min(u0 + b * kThreads, total - 1);   // tail units repeat a valid one
+            const int u = min(u0 + b * NT, total - 1);   // tail units repeat a valid one
             const int i = u / UPC, rem = u % UPC;
             const int h = rem / (D / 4), d = 4 * (rem % (D / 4));
             const int c = list[i];
@@ -457,7 +458,7 @@ __device__ void combine_cells(const AttnArgs &a, const int *list, int n, int g, 
         }
 #pragma unroll
         for (int b = 0; b < kMergeUnits; ++b) {
-            const int u = u0 + b * kThreads;
+            const int u = u0 + b * NT;
             if (u < total) {
                 const int i = u / UPC, rem = u % UPC;
                 const int h = rem / (D / 4), d = 4 * (rem % (D / 4));
@@ -508,7 +509,7 @@ __global__ __launch_bounds__(kThreads) void items_kernel(AttnArgs a) {
         s_list[1] = c;
     }
     __syncthreads();
-    if (s_list[0]) combine_cells<D, G>(a, s_list + 1, 1, g, buf);
+    if (s_list[0]) combine_cells<D, G, kThreads>(a, s_list + 1, 1, g, buf);
 }
 
 // ------------------------------------------------------- bf16, long prompts
@@ -527,35 +528,46 @@ __global__ __launch_bounds__(kThreads) void items_kernel(AttnArgs a) {
 // writes out and lse.  Prompt and generated work of different cells overlap
 // in the one grid.
 
-template <int D>
-constexpr int fused_row_blocks() { return splice::fused_row_blocks(D); }
-
 // Default bound of a generated-row item's wait for the prompt partials: a
 // poll is one agent-scope load (about a microsecond under load) plus a short
 // sleep, so 16384 polls stay around 16 ms -- far beyond any prompt item.
 constexpr int kDefaultWaitPolls = 16384;
 
-// Tiles in flight: the prompt items' register ring and each generated-row
-// wave.  Both fit the register budget of fused_waves_per_simd.
+// Work-group shape: NW waves (splice::fused_waves), NT threads, ROWS rows
+// of a prompt item.  Tiles in flight: the prompt items' register ring and
+// each generated-row wave, within the registers a lane has at
+// WAVES_PER_SIMD waves per SIMD (168 at 3, 256 at 2).
 template <int D>
-constexpr int fused_prompt_depth() { return D <= 128 ? 3 : 2; }
-template <int D>
-constexpr int fused_gen_depth() { return D <= 128 ? 2 : 1; }
-constexpr int fused_waves_per_simd(int D) { return D <= 128 ? 3 : 2; }
+struct Fused {
+    static constexpr int NW = splice::fused_waves(D);
+    static constexpr int NT = NW * 64;
+    static constexpr int RB = splice::fused_row_blocks(D);
+    static constexpr int ROWS = splice::group_rows(D);
+    static constexpr int PROMPT_DEPTH = D <= 128 ? 3 : 2;
+    static constexpr int GEN_DEPTH = D <= 128 ? 2 : 1;
+    static constexpr int WAVES_PER_SIMD = D <= 128 ? 3 : 2;
+    static_assert(ROWS == NW * 16 * RB, "host and device agree on the row groups");
+};
+
+// (m, l) of the prompt slots a generated-row item stages: pairs x prompt
+// chunks x heads, bounded by the host's choice of pairs per item.
+constexpr int kGenStage = splice::kGenStage;
 
 template <int D, int G>
 struct FusedLds {
-    static constexpr int PROMPT = Wide<D, fused_row_blocks<D>()>::LDS;
-    static constexpr int WAVE_MERGE = kWaves * G * (D + 2) * 4;                // waves_merge buffer
-    static constexpr int GEN = cmax(kWaves * WaveMfma<D>::LDS,                  // V^T tiles
-                                    WAVE_MERGE + 2 * kMaxSlots * G * 4);        // + prompt slots' (m, l)
+    static constexpr int NW = Fused<D>::NW;
+    static constexpr int PROMPT = Wide<D, Fused<D>::RB>::LDS;
+    static constexpr int WAVE_MERGE = NW * G * (D + 2) * 4;                     // waves_merge buffer
+    static constexpr int GEN = cmax(NW * WaveMfma<D>::LDS,                      // V^T tiles
+                                    WAVE_MERGE + 2 * kGenStage * 4);            // + prompt slots' (m, l)
     static constexpr int MERGE = 2 * kRowBlock * kMaxSlots * 4;                 // combine_cells staging
     static constexpr int BYTES = cmax(cmax(PROMPT, GEN), MERGE);
+    static_assert(BYTES <= 160 * 1024 - 4096, "fits the LDS of a compute unit");
 };
 
 // Most cells one item can complete: the cells of one row group.
 template <int D, int G>
-constexpr int fused_max_merge() { return Wide<D, fused_row_blocks<D>()>::ROWS / G; }
+constexpr int fused_max_merge() { return Fused<D>::ROWS / G; }
 
 // Each item returns its KV head and leaves in s_list the count and the list
 // of the cells it completed.
@@ -567,7 +579,7 @@ constexpr int fused_max_merge() { return Wide<D, fused_row_blocks<D>()>::ROWS / 
 // last unit (a grid padded to whole rounds of eight) do nothing.
 template <int D, int G>
 __device__ int fused_prompt_item(const AttnArgs &a, int item, char *lds, int *s_list) {
-    constexpr int RB = fused_row_blocks<D>();
+    constexpr int RB = Fused<D>::RB, ROWS = Fused<D>::ROWS;
     using X = Wide<D, RB>;
     const int rg = (item / splice::kXcds) % a.n_rb;
     const int u = (item / splice::kXcds / a.n_rb) * splice::kXcds + item % splice::kXcds;
@@ -585,7 +597,7 @@ __device__ int fused_prompt_item(const AttnArgs &a, int item, char *lds, int *s_
     const int end_cell = clean_group ? a.n_clean : a.C;
     const int grp = clean_group ? rg : rg - a.n_rg_clean;
     static_for<0, RB>([&](auto rb) {
-        const int R = grp * X::ROWS + (wave * RB + rb) * 16 + col;
+        const int R = grp * ROWS + (wave * RB + rb) * 16 + col;
         const int cidx = first_cell + R / G;
         ok[rb] = cidx < end_cell;
         cell[rb] = ok[rb] ? a.order[cidx] : 0;
@@ -619,7 +631,7 @@ __device__ int fused_prompt_item(const AttnArgs &a, int item, char *lds, int *s_
         S.m[rb] = -INFINITY;
         S.lsum[rb] = 0.f;
     });
-    wide_stream<D, RB, fused_prompt_depth<D>()>(L, qb, a.qk_scale, lds, S);
+    wide_stream<D, RB, Fused<D>::PROMPT_DEPTH, Fused<D>::NT>(L, qb, a.qk_scale, lds, S);
 
     const __amdgpu_buffer_rsrc_t r = part_rsrc(a);
     static_for<0, RB>([&](auto rb) {
@@ -639,8 +651,8 @@ __device__ int fused_prompt_item(const AttnArgs &a, int item, char *lds, int *s_
     });
     stores_performed();
     // count this chunk on each cell of the group
-    const int c0 = first_cell + grp * (X::ROWS / G);
-    const int n_cells = min(X::ROWS / G, end_cell - c0);
+    const int c0 = first_cell + grp * (ROWS / G);
+    const int n_cells = min(ROWS / G, end_cell - c0);
     if ((int)threadIdx.x < n_cells) {
         const int c = a.order[c0 + threadIdx.x];
         if (arrive(a, c, g)) s_list[1 + atomicAdd(&s_list[0], 1)] = c;
@@ -649,83 +661,102 @@ __device__ int fused_prompt_item(const AttnArgs &a, int item, char *lds, int *s_
     return g;
 }
 
-// Generated-row item.  After streaming, thread 0 polls the (cell, KV head)
-// counter until every prompt chunk has stored its partial (at most
-// a.wait_polls polls; prompt items have lower block indices and never wait,
-// so they are dispatched first and finish).  Then this item merges in place:
-// its own partial is the last slot and never leaves the chip.  Past the
-// bound it stores its partial and counts itself like any other item, and the
-// last arrival merges.
+// Generated-row item: KV head g and P = a.gen_pairs consecutive cells, wpp =
+// NW / P waves per (cell, KV head) pair streaming that cell's generated rows
+// (interleaved tiles).  After streaming, thread 0 polls the pairs' counters
+// until every prompt chunk has stored its partial (at most a.wait_polls polls
+// in all; prompt items have lower block indices and never wait, so they are
+// dispatched first and finish).  Then this item merges in place: its own
+// partial is the last slot and never leaves the chip.  Past the bound it
+// stores its partials and counts itself like any other item, and the last
+// arrival merges.
 template <int D, int G>
 __device__ int fused_gen_item(const AttnArgs &a, int item, char *lds, int *s_list) {
     using W = WaveMfma<D>;
+    constexpr int NW = Fused<D>::NW, NT = Fused<D>::NT;
+    const int P = a.gen_pairs, wpp = NW / P;
     const int g = item % a.Hkv;
-    const int c = item / a.Hkv;
+    const int c0 = (item / a.Hkv) * P;
+    const int n_pairs = min(P, a.C - c0);
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int c = c0 + wave / wpp;   // this wave's cell
+    const bool valid = c < a.C;
     const int col = threadIdx.x & 15;
     bf16x8_t qb[W::NDS];
-    load_q_cols<D>(a.q + ((size_t)c * a.Hq + (size_t)g * G + col % G) * W::ROW, qb);
-    const size_t goff = (((size_t)c * a.Hkv + g) * (size_t)a.cap + a.i0) * W::ROW;
+    load_q_cols<D>(valid ? a.q + ((size_t)c * a.Hq + (size_t)g * G + col % G) * W::ROW : nullptr, qb);
     KeyList L;
     list_init(L);
-    list_add(L, a.gk + goff, a.gv + goff, a.n_gen);
+    if (valid) {
+        const size_t goff = (((size_t)c * a.Hkv + g) * (size_t)a.cap + a.i0) * W::ROW;
+        list_add(L, a.gk + goff, a.gv + goff, a.n_gen);
+    }
     WaveState<D> S;
     state_init(S);
     const ColMask cm{true, true, true};
-    wave_stream<D, fused_gen_depth<D>(), kGenAux>(L, wave, kWaves, cm, qb, a.qk_scale, lds + wave * W::LDS, S);
+    wave_stream<D, Fused<D>::GEN_DEPTH, kGenAux>(L, wave % wpp, wpp, cm, qb, a.qk_scale, lds + wave * W::LDS, S);
     state_finish(S);
 
-    int *cnt = a.counters + c * a.Hkv + g;
     if (threadIdx.x == 0) {
-        bool ready = a.n_p == 0;
-        for (int i = 0; !ready && i < a.wait_polls; ++i) {
-            ready = __hip_atomic_load(cnt, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) >= a.n_p;
-            if (!ready) __builtin_amdgcn_s_sleep(4);
+        bool ready = true;
+        int polls = 0;
+        for (int q = 0; q < n_pairs && ready; ++q) {
+            const int *cnt = a.counters + (c0 + q) * a.Hkv + g;
+            bool done = a.n_p == 0;
+            while (!done && polls < a.wait_polls) {
+                done = __hip_atomic_load(cnt, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) >= a.n_p;
+                if (!done) {
+                    __builtin_amdgcn_s_sleep(4);
+                    ++polls;
+                }
+            }
+            ready = done;
         }
         s_list[0] = ready ? -1 : 0;
     }
     __syncthreads();   // also: every wave is done with its V^T tile
     const bool ready = s_list[0] < 0;
     const __amdgpu_buffer_rsrc_t r = part_rsrc(a);
-    const uint32_t base = slot_off(a, c, g, 0);
     const uint32_t slot_bytes = (uint32_t)a.slot_floats * 4u;
     if (ready) {
-        // stage the prompt slots' (m, l) behind the wave-merge buffer
+        // stage the prompt slots' (m, l) of every pair behind the wave-merge buffer
         float *s_pm = reinterpret_cast<float *>(lds + FusedLds<D, G>::WAVE_MERGE);
-        float *s_pl = s_pm + kMaxSlots * G;
-        for (int t = threadIdx.x; t < a.n_p * G; t += kThreads) {
-            const uint32_t off = base + (uint32_t)(t / G) * slot_bytes;
-            s_pm[t] = part_load1(r, off + (uint32_t)(G * D + t % G) * 4u);
-            s_pl[t] = part_load1(r, off + (uint32_t)(G * D + G + t % G) * 4u);
+        float *s_pl = s_pm + kGenStage;
+        const int per_pair = a.n_p * G;
+        for (int t = threadIdx.x; t < n_pairs * per_pair; t += NT) {
+            const int q = t / per_pair, k = (t % per_pair) / G, h = t % G;
+            const uint32_t off = slot_off(a, c0 + q, g, k);
+            s_pm[t] = part_load1(r, off + (uint32_t)(G * D + h) * 4u);
+            s_pl[t] = part_load1(r, off + (uint32_t)(G * D + G + h) * 4u);
         }
-        const bool zero_term = has_zero_term(a, c);
-        waves_merge<D, G>(S, lds, [&](int h, int d, float Mg, float Lg, f32x4_t Og) {
+        waves_merge<D, G, NW>(S, lds, wpp, n_pairs, [&](int q, int h, int d, float Mg, float Lg, f32x4_t Og) {
+            const int cq = c0 + q;
+            const float *pm = s_pm + q * per_pair + h, *pl = s_pl + q * per_pair + h;
+            const uint32_t base = slot_off(a, cq, g, 0) + (uint32_t)(h * D + d) * 4u;
+            const bool zero_term = has_zero_term(a, cq);
             float M = zero_term ? 0.f : -INFINITY;
-            for (int k = 0; k < a.n_p; ++k) M = fmaxf(M, s_pm[k * G + h]);
+            for (int k = 0; k < a.n_p; ++k) M = fmaxf(M, pm[k * G]);
             M = fmaxf(M, Mg);
             float Ls = zero_term ? (float)(a.sb - a.sa) * fast_exp2(-M) : 0.f;
             f32x4_t O = {0.f, 0.f, 0.f, 0.f};
-            constexpr int B = 8;
+            constexpr int B = 4;
             for (int k0 = 0; k0 < a.n_p; k0 += B) {
                 f32x4_t ok[B];
 #pragma unroll
-                for (int j = 0; j < B; ++j)
-                    ok[j] = part_load4(r, base + (uint32_t)min(k0 + j, a.n_p - 1) * slot_bytes +
-                                              (uint32_t)(h * D + d) * 4u);
+                for (int j = 0; j < B; ++j) ok[j] = part_load4(r, base + (uint32_t)min(k0 + j, a.n_p - 1) * slot_bytes);
 #pragma unroll
                 for (int j = 0; j < B; ++j)
-                    if (k0 + j < a.n_p) fold_slot(s_pm[(k0 + j) * G + h], s_pl[(k0 + j) * G + h], ok[j], M, Ls, O);
+                    if (k0 + j < a.n_p) fold_slot(pm[(k0 + j) * G], pl[(k0 + j) * G], ok[j], M, Ls, O);
             }
             fold_slot(Mg, Lg, Og, M, Ls, O);   // this item's slot, a.n_p, comes last
-            write_row(a, c * a.Hq + g * G + h, d, D, M, Ls, O);
+            write_row(a, cq * a.Hq + g * G + h, d, D, M, Ls, O);
         });
-        if (threadIdx.x == 0) {
-            __hip_atomic_store(cnt, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            s_list[0] = 0;   // nothing left to merge
-        }
+        if ((int)threadIdx.x < n_pairs)
+            __hip_atomic_store(a.counters + (c0 + threadIdx.x) * a.Hkv + g, 0, __ATOMIC_RELAXED,
+                               __HIP_MEMORY_SCOPE_AGENT);
+        if (threadIdx.x == 0) s_list[0] = 0;   // nothing left to merge
     } else {
-        const uint32_t slot = slot_off(a, c, g, a.n_p);
-        waves_merge<D, G>(S, lds, [&](int h, int d, float M, float Lsum, f32x4_t O) {
+        waves_merge<D, G, NW>(S, lds, wpp, n_pairs, [&](int q, int h, int d, float M, float Lsum, f32x4_t O) {
+            const uint32_t slot = slot_off(a, c0 + q, g, a.n_p);
             part_store4(r, slot + (uint32_t)(h * D + d) * 4u, O);
             if (d == 0) {
                 part_store1(r, slot + (uint32_t)(G * D + h) * 4u, M);
@@ -733,22 +764,20 @@ __device__ int fused_gen_item(const AttnArgs &a, int item, char *lds, int *s_lis
             }
         });
         stores_performed();
-        if (threadIdx.x == 0 && arrive(a, c, g)) {
-            s_list[0] = 1;
-            s_list[1] = c;
-        }
+        if ((int)threadIdx.x < n_pairs && arrive(a, c0 + threadIdx.x, g))
+            s_list[1 + atomicAdd(&s_list[0], 1)] = c0 + threadIdx.x;
     }
     __syncthreads();
     return g;
 }
 
 template <int D, int G>
-__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(fused_waves_per_simd(D))))
+__global__ __launch_bounds__(Fused<D>::NT) __attribute__((amdgpu_waves_per_eu(Fused<D>::WAVES_PER_SIMD)))
 void fused_kernel(AttnArgs a) {
     __shared__ __attribute__((aligned(16))) char lds[FusedLds<D, G>::BYTES];
     constexpr int MAXM = fused_max_merge<D, G>();
     __shared__ int s_list[1 + MAXM];   // [0] count, [1..] cells to merge
-    static_assert(MAXM <= kThreads, "one thread per cell of a row group");
+    static_assert(MAXM <= Fused<D>::NT, "one thread per cell of a row group");
     if (threadIdx.x == 0) s_list[0] = 0;
     __syncthreads();
     const int g = (int)blockIdx.x < a.n_prompt_items
@@ -758,7 +787,7 @@ void fused_kernel(AttnArgs a) {
     // merge in batches whose (m, l) staging fits
     const int per = max(1, (kRowBlock * kMaxSlots) / (a.n_slots * G));
     for (int i = 0; i < n; i += per) {
-        combine_cells<D, G>(a, s_list + 1 + i, min(per, n - i), g, lds);
+        combine_cells<D, G, Fused<D>::NT>(a, s_list + 1 + i, min(per, n - i), g, lds);
         __syncthreads();
     }
 }

@@ -117,16 +117,18 @@ constexpr int kRowBlock = 64;              // rows of the f32 merge staging
 constexpr int kMinChunk = 256;             // a default chunk is at least this long
 constexpr int kMaxChunks = 32;             // default chunks per part (prompt, generated)
 constexpr int kMaxSlots = 64;              // partial results per (cell, KV head)
+constexpr int kGenStage = 4096;            // bf16: (m, l) pairs x chunks x heads a generated item stages
 constexpr int kPromptItemsTarget = 512;    // f32 prompt items a default split aims for
 constexpr int kGenItemsTarget = 2048;      // f32 generated items a default split aims for
 constexpr int kWideItemsTarget = 512;      // bf16 prompt work groups a default split aims for
 constexpr int kWideMinChunk = 128;         // a default bf16 prompt chunk is at least this long
 
-// bf16 prompt items: 16-row MFMA blocks per wave (a wave's output
-// accumulators, RB * D / 4 registers, stay at 32 for D <= 128) and rows per
-// work group (four waves).
-constexpr int fused_row_blocks(int D) { return D <= 64 ? 2 : 1; }
-constexpr int group_rows(int D) { return 4 * 16 * fused_row_blocks(D); }
+// bf16 items: waves per work group, 16-row MFMA blocks per wave (a wave's
+// output accumulators, RB * D / 4 registers, stay at 32 for D <= 128) and
+// rows per prompt item.
+constexpr int fused_waves(int) { return 4; }
+constexpr int fused_row_blocks(int) { return 1; }
+constexpr int group_rows(int D) { return fused_waves(D) * 16 * fused_row_blocks(D); }
 
 // Work groups are handed to the GPU's eight XCDs in turn (block b to XCD
 // b mod 8); the bf16 prompt grid is laid out in rounds of this many blocks.
@@ -208,7 +210,23 @@ struct AttnPlan {
     int n_g, g_len;          // chunks over the visible generated rows
     int n_slots;             // partial results per (cell, KV head)
     int n_prompt_items, n_gen_items;
+    int gen_pairs;           // bf16: (cell, KV head) pairs per generated-row work group
 };
+
+// bf16 generated-row items: a work group of fused_waves(D) waves serves P
+// consecutive cells of one KV head, NW / P waves each.  Each wave should
+// stream at least two 16-row tiles, so short generated parts pack many
+// cells into a work group and long ones spread one cell over all waves.
+// The staging of the pairs' prompt (m, l) bounds P.
+inline int gen_pairs(const splice_shape &sh, int n_gen, int n_p) {
+    const int nw = fused_waves(sh.head_dim);
+    const int tiles = ceil_div(n_gen, 16);
+    int wpp = nw;
+    while (wpp > 1 && tiles < 2 * wpp) wpp /= 2;
+    int P = nw / wpp;
+    while (P > 1 && P * n_p * group_of(sh) > kGenStage) P /= 2;
+    return P;
+}
 
 // Cells of the call that are not spliced.
 inline int count_clean(const splice_shape &sh, const splice_call &call, const int32_t *cell_LW) {
@@ -226,12 +244,13 @@ inline AttnPlan plan_attn(const splice_shape &sh, const splice_call &call, int n
         p.p_len = p.g_len = 64;
         p.n_slots = 0;
         p.n_prompt_items = p.n_gen_items = 0;
+        p.gen_pairs = 1;
         return p;
     }
     cut(p.geo.n_prompt, prompt_chunk_target(sh), call.split_keys, &p.n_p, &p.p_len,
         bf16_path(sh) ? kWideMinChunk : kMinChunk);
     if (bf16_path(sh)) {
-        // one generated-row item per (cell, KV head), its four waves merged
+        // one generated-row partial per (cell, KV head)
         p.n_g = 1;
         p.g_len = p.geo.n_gen;
     } else {
@@ -244,7 +263,13 @@ inline AttnPlan plan_attn(const splice_shape &sh, const splice_call &call, int n
     } else {
         p.n_prompt_items = prompt_items_per_chunk(sh, n_clean) * p.n_p;
     }
-    p.n_gen_items = sh.n_cells * sh.n_kv_heads * p.n_g;
+    if (bf16_path(sh)) {
+        p.gen_pairs = gen_pairs(sh, p.geo.n_gen, p.n_p);
+        p.n_gen_items = ceil_div(sh.n_cells, p.gen_pairs) * sh.n_kv_heads;
+    } else {
+        p.gen_pairs = 1;
+        p.n_gen_items = sh.n_cells * sh.n_kv_heads * p.n_g;
+    }
     return p;
 }
 

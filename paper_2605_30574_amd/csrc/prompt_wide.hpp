@@ -1,7 +1,7 @@
 // prompt_wide.hpp -- the shared-prompt contraction: many (cell, q head) rows
 // of one KV head against the same prompt tiles, on the matrix cores.
 //
-// A work group of four waves owns wide_rows(D) rows; each wave owns RB blocks
+// A work group of NW waves owns NW * 16 * RB rows; each wave owns RB blocks
 // of 16 rows.  A 32-key tile of the prompt (K row-major, V transposed) is
 // staged in LDS once per work group and then, per wave,
 //   S  = K Q^T  : the K operand (16 keys x 32 d) is read from LDS once and
@@ -23,7 +23,6 @@ namespace splice_dev {
 template <int D, int RB_>
 struct Wide {
     static constexpr int RB = RB_;                          // 16-row blocks per wave
-    static constexpr int ROWS = 4 * 16 * RB;                // rows per work group
     static constexpr int TK = 32;                           // keys per tile
     static constexpr int ROW = D * 2;                       // bytes per K or V row
     static constexpr int NDS = D / 32;                      // k-steps of q.k
@@ -33,34 +32,44 @@ struct Wide {
     static constexpr int KTILE = TK * KROW;
     static constexpr int BUF = KTILE + D * VROW;            // one staged tile
     static constexpr int LDS = 2 * BUF;                     // double buffer
-    static constexpr int NKU = TK * (D / 8) / kThreads;     // 16-byte K units per thread
-    static constexpr int VU = (D / 8) * (TK / 2);           // V units: 2 keys x 8 d
-    static constexpr int NVU = (VU + kThreads - 1) / kThreads;   // V units per thread
-    static_assert(NKU >= 1 && NVU <= 2, "tile staging assumes 64 <= D <= 256");
+};
+
+// How NT threads share the loads of one tile: KU 16-byte K units (unit u is
+// bytes 16 (u mod D/8) of key row u / (D/8)) owned by threads 0, 1, ...;
+// VU V units of 2 keys x 8 d (keys 2 kp, 2 kp + 1 with kp = u mod 16, bytes
+// 16 dg with dg = u / 16) owned by the last VU threads (all threads in
+// turn when VU >= NT), so that a thread owning both is rare.
+template <int D, int NT>
+struct TileShare {
+    static constexpr int KU = Wide<D, 1>::TK * (D / 8);
+    static constexpr int VU = (D / 8) * (Wide<D, 1>::TK / 2);
+    static constexpr int NKU = (KU + NT - 1) / NT;
+    static constexpr int NVU = (VU + NT - 1) / NT;
+    static constexpr int VSHIFT = VU < NT ? NT - VU : 0;
+    static_assert(NVU <= 2 && NKU <= 4, "tile staging assumes 64 <= D <= 256");
 };
 
 // One thread's share of a tile in flight.
-template <int D>
+template <int D, int NT>
 struct WideRegs {
-    u32x4_t k[Wide<D, 1>::NKU];
-    u32x4_t v[Wide<D, 1>::NVU][2];
+    u32x4_t k[TileShare<D, NT>::NKU];
+    u32x4_t v[TileShare<D, NT>::NVU][2];
 };
 
-// K: unit u is 16 bytes of key row u / (D / 8).  V: unit u holds keys
-// 2 kp, 2 kp + 1 (kp = u mod 16) at bytes 16 dg .. 16 dg + 15 (dg = u / 16).
-template <int D>
-__device__ __forceinline__ void wide_fetch(const TileRef &t, WideRegs<D> &r) {
+template <int D, int NT>
+__device__ __forceinline__ void wide_fetch(const TileRef &t, WideRegs<D, NT> &r) {
     using X = Wide<D, 1>;
+    using T = TileShare<D, NT>;
     const int tid = threadIdx.x;
     const __amdgpu_buffer_rsrc_t rk = rows_rsrc(t.k, t.n * X::ROW);
     const __amdgpu_buffer_rsrc_t rv = rows_rsrc(t.v, t.n * X::ROW);
-    static_for<0, X::NKU>([&](auto i) {
-        const int u = tid + kThreads * i;
-        r.k[i] = row_load<0>(rk, (u / (D / 8)) * X::ROW + (u % (D / 8)) * 16);
+    static_for<0, T::NKU>([&](auto i) {
+        const int u = tid + NT * i;
+        if (T::KU % NT == 0 || u < T::KU) r.k[i] = row_load<0>(rk, (u / (D / 8)) * X::ROW + (u % (D / 8)) * 16);
     });
-    static_for<0, X::NVU>([&](auto i) {
-        const int u = tid + kThreads * i;
-        if (X::VU % kThreads == 0 || u < X::VU) {
+    static_for<0, T::NVU>([&](auto i) {
+        const int u = tid - T::VSHIFT + NT * i;
+        if ((T::VSHIFT == 0 && T::VU % NT == 0) || (u >= 0 && u < T::VU)) {
             const int kp = u & 15, dg = u >> 4;
             r.v[i][0] = row_load<0>(rv, (2 * kp) * X::ROW + 16 * dg);
             r.v[i][1] = row_load<0>(rv, (2 * kp + 1) * X::ROW + 16 * dg);
@@ -71,19 +80,21 @@ __device__ __forceinline__ void wide_fetch(const TileRef &t, WideRegs<D> &r) {
 // K row-major (16-byte units), V transposed: row d holds the tile's keys.
 // The 16 lanes of one dg fill a 64-byte V^T row segment; the four dg of a
 // wave land 8 rows apart, 16 banks apart.
-template <int D>
-__device__ __forceinline__ void wide_stage(const WideRegs<D> &r, char *buf) {
+template <int D, int NT>
+__device__ __forceinline__ void wide_stage(const WideRegs<D, NT> &r, char *buf) {
     using X = Wide<D, 1>;
+    using T = TileShare<D, NT>;
     const int tid = threadIdx.x;
     char *sK = buf;
     char *sV = buf + X::KTILE;
-    static_for<0, X::NKU>([&](auto i) {
-        const int u = tid + kThreads * i;
-        *reinterpret_cast<u32x4_t *>(sK + (u / (D / 8)) * X::KROW + (u % (D / 8)) * 16) = r.k[i];
+    static_for<0, T::NKU>([&](auto i) {
+        const int u = tid + NT * i;
+        if (T::KU % NT == 0 || u < T::KU)
+            *reinterpret_cast<u32x4_t *>(sK + (u / (D / 8)) * X::KROW + (u % (D / 8)) * 16) = r.k[i];
     });
-    static_for<0, X::NVU>([&](auto i) {
-        const int u = tid + kThreads * i;
-        if (X::VU % kThreads == 0 || u < X::VU) {
+    static_for<0, T::NVU>([&](auto i) {
+        const int u = tid - T::VSHIFT + NT * i;
+        if ((T::VSHIFT == 0 && T::VU % NT == 0) || (u >= 0 && u < T::VU)) {
             const int kp = u & 15, dg = u >> 4;
             static_for<0, 8>([&](auto j) {
                 constexpr int jj = decltype(j)::value;
@@ -176,30 +187,19 @@ __device__ __forceinline__ void wide_compute(const char *buf, int n_valid,
     });
 }
 
-// Tiles a work group keeps in flight: fetched into registers DEPTH - 1 tiles
-// ahead of the one being computed (the LDS tiles are double-buffered).
-template <int D>
-constexpr int wide_depth() { return D <= 128 ? 3 : 2; }
-
-// Stream every tile of the work group's list.  Iteration t computes the LDS
-// buffer t & 1, stages tile t + 1 from registers into the other buffer and
-// refills the freed registers with tile t + DEPTH; one barrier per tile
-// orders the buffers.  The loop is unrolled DEPTH times so that the register
-// sets are only ever indexed by constants.  Called by all threads of the
-// work group.
-template <int D, int RB, int DEPTH>
+template <int D, int RB, int DEPTH, int NT>
 __device__ __forceinline__ void wide_stream(const KeyList &L, const bf16x8_t (&qb)[RB][Wide<D, RB>::NDS],
                                             float qk_scale, char *lds, WideState<D, RB> &S) {
     using X = Wide<D, RB>;
     const int n_tiles = list_tiles(L);
     if (n_tiles == 0) return;
-    WideRegs<D> r[DEPTH];
+    WideRegs<D, NT> r[DEPTH];
     TileRef ref[DEPTH];
     static_for<0, DEPTH>([&](auto i) {
         ref[i] = list_tile_or_empty<X::TK>(L, i, n_tiles, X::ROW);
-        wide_fetch<D>(ref[i], r[i]);
+        wide_fetch<D, NT>(ref[i], r[i]);
     });
-    wide_stage<D>(r[0], lds);
+    wide_stage<D, NT>(r[0], lds);
     __syncthreads();
     for (int base = 0; base < n_tiles; base += DEPTH) {
         static_for<0, DEPTH>([&](auto j) {
@@ -211,10 +211,10 @@ __device__ __forceinline__ void wide_stream(const KeyList &L, const bf16x8_t (&q
             // with tile t + DEPTH, or an empty tile past the end, on every
             // path, so the count of loads in flight never depends on `live`
             ref[j] = list_tile_or_empty<X::TK>(L, t + DEPTH, n_tiles, X::ROW);
-            wide_fetch<D>(ref[j], r[j]);
+            wide_fetch<D, NT>(ref[j], r[j]);
             if (live) {
                 wide_compute<D, RB>(lds + (t & 1) * X::BUF, cur.n, qb, qk_scale, S);
-                if (t + 1 < n_tiles) wide_stage<D>(r[jn], lds + ((t + 1) & 1) * X::BUF);
+                if (t + 1 < n_tiles) wide_stage<D, NT>(r[jn], lds + ((t + 1) & 1) * X::BUF);
                 __syncthreads();   // the next buffer is staged; nobody reads this one any more
             }
         });

@@ -281,6 +281,7 @@ int32_t splice_decode_attn(const splice_shape *shape, const splice_call *call, c
     a.n_rb = splice::bf16_path(sh) ? splice::row_groups(sh, n_clean) : 0;
     a.n_rg_clean = splice::bf16_path(sh) ? splice::clean_row_groups(sh, n_clean) : 0;
     a.n_prompt_items = plan.n_prompt_items;
+    a.gen_pairs = plan.gen_pairs;
     a.wait_polls = call->merge_wait == 0 ? kDefaultWaitPolls : (call->merge_wait < 0 ? 0 : call->merge_wait);
     a.qk_scale = call->scale * kLog2e;
     fill_mask(sh, *call, cell_LW, a.spliced);
@@ -300,7 +301,8 @@ int32_t splice_decode_attn(const splice_shape *shape, const splice_call *call, c
     }
     const int64_t items = (int64_t)plan.n_prompt_items + plan.n_gen_items;
     if (items > INT32_MAX) return SPLICE_EUNSUPPORTED;
-    hipLaunchKernelGGL(kern.items, dim3((unsigned)items), dim3(kThreads), 0, (hipStream_t)stream, a);
+    const int threads = splice::bf16_path(sh) ? 64 * splice::fused_waves(sh.head_dim) : kThreads;
+    hipLaunchKernelGGL(kern.items, dim3((unsigned)items), dim3((unsigned)threads), 0, (hipStream_t)stream, a);
     return launch_status();
 }
 

@@ -327,17 +327,18 @@ __device__ __forceinline__ void state_finish(WaveState<D> &S) {
     S.lsum += __shfl_xor(S.lsum, 32);
 }
 
-// Merge the waves of a work group (each with its WaveState, finished, the
-// same G heads in columns j mod G) through LDS and hand every group of four
-// consecutive outputs of each head to sink(h, d, M, L, O) -- M and L in
-// base-2 units, O not yet divided by L.  `buf` needs kWaves * G * (D + 2)
-// floats and may alias the V^T tiles.
-template <int D, int G, typename Sink>
-__device__ __forceinline__ void waves_merge(WaveState<D> &S, char *buf, Sink sink) {
+// Merge the waves of a work group in groups of wpp consecutive waves (each
+// wave with its WaveState, finished; a group's waves stream the same G heads,
+// in columns j mod G) through LDS, and hand every group of four consecutive
+// outputs of head h of group p < n_groups to sink(p, h, d, M, L, O) -- M and
+// L in base-2 units, O not yet divided by L.  `buf` needs NW * G * (D + 2)
+// floats and may alias the V^T tiles.  Called by all threads.
+template <int D, int G, int NW, typename Sink>
+__device__ __forceinline__ void waves_merge(WaveState<D> &S, char *buf, int wpp, int n_groups, Sink sink) {
     using W = WaveMfma<D>;
-    float *s_o = reinterpret_cast<float *>(buf);          // [kWaves][G][D]
-    float *s_m = s_o + kWaves * G * D;                      // [kWaves][G]
-    float *s_l = s_m + kWaves * G;                          // [kWaves][G]
+    float *s_o = reinterpret_cast<float *>(buf);          // [NW][G][D]
+    float *s_m = s_o + NW * G * D;                          // [NW][G]
+    float *s_l = s_m + NW * G;                              // [NW][G]
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int col = lane & 15, quad = lane >> 4;
     __syncthreads();   // every wave is done with its V^T tile
@@ -351,21 +352,21 @@ __device__ __forceinline__ void waves_merge(WaveState<D> &S, char *buf, Sink sin
         }
     }
     __syncthreads();
-    for (int e = tid; e < G * D / 4; e += kThreads) {
-        const int h = e / (D / 4), d = 4 * (e % (D / 4));
+    constexpr int UPG = G * D / 4;   // units of four outputs per group
+    for (int e = tid; e < n_groups * UPG; e += NW * 64) {
+        const int p = e / UPG, h = (e % UPG) / (D / 4), d = 4 * (e % (D / 4));
+        const int w0 = p * wpp;
         float M = -INFINITY;
-#pragma unroll
-        for (int w = 0; w < kWaves; ++w) M = fmaxf(M, s_m[w * G + h]);
+        for (int w = w0; w < w0 + wpp; ++w) M = fmaxf(M, s_m[w * G + h]);
         const float Ms = M == -INFINITY ? 0.f : M;
         float L = 0.f;
         f32x4_t O = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int w = 0; w < kWaves; ++w) {
+        for (int w = w0; w < w0 + wpp; ++w) {
             const float f = fast_exp2(s_m[w * G + h] - Ms);
             L = fmaf(s_l[w * G + h], f, L);
             O += *reinterpret_cast<const f32x4_t *>(s_o + (w * G + h) * D + d) * f;
         }
-        sink(h, d, M, L, O);
+        sink(p, h, d, M, L, O);
     }
 }
 
