@@ -514,19 +514,21 @@ __global__ __launch_bounds__(kThreads) void items_kernel(AttnArgs a) {
 
 // ------------------------------------------------------- bf16, long prompts
 //
-// One launch per call.  Blocks [0, n_prompt_items) are shared-prompt items
-// (prompt_wide.hpp): work group = (KV head, group of Wide::ROWS rows, prompt
-// chunk), where the rows of a KV head are the (cell, q head) pairs of every
-// cell, unspliced cells first, and a group holds rows of one class only.
-// Each K/V tile of the chunk is staged in LDS once for all of the group's
-// rows, and every row gets one partial result.  The other blocks are
-// generated-row items: one work group per (cell, KV head) streams the cell's
-// generated rows (four waves, interleaved tiles) and merges its waves into
-// one more partial.  Every item then counts itself on the (cell, KV head)
-// pairs it fed; the item that completes a pair merges its partials (slot
-// order: prompt chunks, then the generated rows; then the ZERO term) and
-// writes out and lse.  Prompt and generated work of different cells overlap
-// in the one grid.
+// One launch per call, two kinds of work group:
+//   shared-prompt items (prompt_wide.hpp), work group = (KV head, group of
+//     Fused::ROWS rows, prompt chunk), where the rows of a KV head are the
+//     (cell, q head) pairs of every cell, unspliced cells first, and a group
+//     holds rows of one class only -- each K/V tile of the chunk is staged
+//     in LDS once for all of the group's rows, and every row gets one
+//     partial result;
+//   generated-row items, work group = (KV head, a few consecutive cells),
+//     whose waves stream each cell's generated rows into one more partial;
+//     the item waits for the prompt partials of its cells and merges them
+//     (slot order: prompt chunks, then the generated rows; then the ZERO
+//     term) into out and lse.
+// Blocks [0, n_prompt_items) are the prompt items.  Work groups start in
+// block order, so the prompt items a generated-row item waits for have
+// started before it.
 
 // Default bound of a generated-row item's wait for the prompt partials: a
 // poll is one agent-scope load (about a microsecond under load) plus a short
@@ -549,17 +551,15 @@ struct Fused {
     static_assert(ROWS == NW * 16 * RB, "host and device agree on the row groups");
 };
 
-// (m, l) of the prompt slots a generated-row item stages: pairs x prompt
-// chunks x heads, bounded by the host's choice of pairs per item.
-constexpr int kGenStage = splice::kGenStage;
+// Prompt slots a generated-row item loads in one round for its merge.
+constexpr int kMergeBatch = 8;
 
 template <int D, int G>
 struct FusedLds {
     static constexpr int NW = Fused<D>::NW;
     static constexpr int PROMPT = Wide<D, Fused<D>::RB>::LDS;
     static constexpr int WAVE_MERGE = NW * G * (D + 2) * 4;                     // waves_merge buffer
-    static constexpr int GEN = cmax(NW * WaveMfma<D>::LDS,                      // V^T tiles
-                                    WAVE_MERGE + 2 * kGenStage * 4);            // + prompt slots' (m, l)
+    static constexpr int GEN = cmax(NW * WaveMfma<D>::LDS, WAVE_MERGE);         // V^T tiles, wave merge
     static constexpr int MERGE = 2 * kRowBlock * kMaxSlots * 4;                 // combine_cells staging
     static constexpr int BYTES = cmax(cmax(PROMPT, GEN), MERGE);
     static_assert(BYTES <= 160 * 1024 - 4096, "fits the LDS of a compute unit");
@@ -570,22 +570,22 @@ template <int D, int G>
 constexpr int fused_max_merge() { return Fused<D>::ROWS / G; }
 
 // Each item returns its KV head and leaves in s_list the count and the list
-// of the cells it completed.
+// of the cells it completed (a merge handed over by a generated-row item).
 //
-// Block b of the prompt part serves unit u = (KV head, chunk) and row group
-// rg with b mod 8 = u mod 8: work groups are handed to the eight XCDs in
-// turn, so every row group of a unit runs on one XCD and the unit's tiles
-// come from that XCD's L2 after the first read.  Blocks with u past the
-// last unit (a grid padded to whole rounds of eight) do nothing.
+// Work groups are handed to the eight XCDs in turn (block b to XCD b mod
+// 8).  Prompt block b serves unit u = (KV head, chunk) and row group rg with
+// b mod 8 = u mod 8, so every row group of a unit runs on one XCD and the
+// unit's tiles come from that XCD's L2 after the first read.  Blocks with u
+// past the last unit (a grid padded to whole rounds of eight) do nothing.
 template <int D, int G>
 __device__ int fused_prompt_item(const AttnArgs &a, int item, char *lds, int *s_list) {
     constexpr int RB = Fused<D>::RB, ROWS = Fused<D>::ROWS;
+    constexpr int X8 = splice::kXcds;
     using X = Wide<D, RB>;
-    const int rg = (item / splice::kXcds) % a.n_rb;
-    const int u = (item / splice::kXcds / a.n_rb) * splice::kXcds + item % splice::kXcds;
+    const int rg = (item / X8) % a.n_rb;
+    const int u = (item / X8 / a.n_rb) * X8 + item % X8;
     if (u >= a.n_p * a.Hkv) return 0;   // s_list[0] stays 0: nothing to merge
-    const int pk = u % a.n_p;
-    const int g = u / a.n_p;
+    const int g = u / a.n_p, pk = u % a.n_p;
     const int lane = threadIdx.x & 63, col = lane & 15, quad = lane >> 4;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     bf16x8_t qb[RB][X::NDS];
@@ -673,7 +673,7 @@ __device__ int fused_prompt_item(const AttnArgs &a, int item, char *lds, int *s_
 template <int D, int G>
 __device__ int fused_gen_item(const AttnArgs &a, int item, char *lds, int *s_list) {
     using W = WaveMfma<D>;
-    constexpr int NW = Fused<D>::NW, NT = Fused<D>::NT;
+    constexpr int NW = Fused<D>::NW;
     const int P = a.gen_pairs, wpp = NW / P;
     const int g = item % a.Hkv;
     const int c0 = (item / a.Hkv) * P;
@@ -718,34 +718,55 @@ __device__ int fused_gen_item(const AttnArgs &a, int item, char *lds, int *s_lis
     const __amdgpu_buffer_rsrc_t r = part_rsrc(a);
     const uint32_t slot_bytes = (uint32_t)a.slot_floats * 4u;
     if (ready) {
-        // stage the prompt slots' (m, l) of every pair behind the wave-merge buffer
-        float *s_pm = reinterpret_cast<float *>(lds + FusedLds<D, G>::WAVE_MERGE);
-        float *s_pl = s_pm + kGenStage;
-        const int per_pair = a.n_p * G;
-        for (int t = threadIdx.x; t < n_pairs * per_pair; t += NT) {
-            const int q = t / per_pair, k = (t % per_pair) / G, h = t % G;
-            const uint32_t off = slot_off(a, c0 + q, g, k);
-            s_pm[t] = part_load1(r, off + (uint32_t)(G * D + h) * 4u);
-            s_pl[t] = part_load1(r, off + (uint32_t)(G * D + G + h) * 4u);
-        }
         waves_merge<D, G, NW>(S, lds, wpp, n_pairs, [&](int q, int h, int d, float Mg, float Lg, f32x4_t Og) {
             const int cq = c0 + q;
-            const float *pm = s_pm + q * per_pair + h, *pl = s_pl + q * per_pair + h;
-            const uint32_t base = slot_off(a, cq, g, 0) + (uint32_t)(h * D + d) * 4u;
+            const uint32_t sbase = slot_off(a, cq, g, 0);
+            const uint32_t o_off = (uint32_t)(h * D + d) * 4u;
+            const uint32_t m_off = (uint32_t)(G * D + h) * 4u, l_off = (uint32_t)(G * D + G + h) * 4u;
             const bool zero_term = has_zero_term(a, cq);
             float M = zero_term ? 0.f : -INFINITY;
-            for (int k = 0; k < a.n_p; ++k) M = fmaxf(M, pm[k * G]);
-            M = fmaxf(M, Mg);
-            float Ls = zero_term ? (float)(a.sb - a.sa) * fast_exp2(-M) : 0.f;
+            float Ls = 0.f;
             f32x4_t O = {0.f, 0.f, 0.f, 0.f};
-            constexpr int B = 4;
-            for (int k0 = 0; k0 < a.n_p; k0 += B) {
+            constexpr int B = kMergeBatch;
+            if (a.n_p <= B) {
+                // one round of loads: every prompt slot's (m, l, o) at once
                 f32x4_t ok[B];
+                float mk[B], lk[B];
 #pragma unroll
-                for (int j = 0; j < B; ++j) ok[j] = part_load4(r, base + (uint32_t)min(k0 + j, a.n_p - 1) * slot_bytes);
+                for (int j = 0; j < B; ++j) {
+                    const uint32_t off = sbase + (uint32_t)min(j, max(a.n_p - 1, 0)) * slot_bytes;
+                    if (j < a.n_p) {
+                        ok[j] = part_load4(r, off + o_off);
+                        mk[j] = part_load1(r, off + m_off);
+                        lk[j] = part_load1(r, off + l_off);
+                    }
+                }
 #pragma unroll
                 for (int j = 0; j < B; ++j)
-                    if (k0 + j < a.n_p) fold_slot(pm[(k0 + j) * G], pl[(k0 + j) * G], ok[j], M, Ls, O);
+                    if (j < a.n_p) M = fmaxf(M, mk[j]);
+                M = fmaxf(M, Mg);
+                if (zero_term) Ls = (float)(a.sb - a.sa) * fast_exp2(-M);
+#pragma unroll
+                for (int j = 0; j < B; ++j)
+                    if (j < a.n_p) fold_slot(mk[j], lk[j], ok[j], M, Ls, O);
+            } else {
+                for (int k = 0; k < a.n_p; ++k) M = fmaxf(M, part_load1(r, sbase + (uint32_t)k * slot_bytes + m_off));
+                M = fmaxf(M, Mg);
+                if (zero_term) Ls = (float)(a.sb - a.sa) * fast_exp2(-M);
+                for (int k0 = 0; k0 < a.n_p; k0 += B) {
+                    f32x4_t ok[B];
+                    float mk[B], lk[B];
+#pragma unroll
+                    for (int j = 0; j < B; ++j) {
+                        const uint32_t off = sbase + (uint32_t)min(k0 + j, a.n_p - 1) * slot_bytes;
+                        ok[j] = part_load4(r, off + o_off);
+                        mk[j] = part_load1(r, off + m_off);
+                        lk[j] = part_load1(r, off + l_off);
+                    }
+#pragma unroll
+                    for (int j = 0; j < B; ++j)
+                        if (k0 + j < a.n_p) fold_slot(mk[j], lk[j], ok[j], M, Ls, O);
+                }
             }
             fold_slot(Mg, Lg, Og, M, Ls, O);   // this item's slot, a.n_p, comes last
             write_row(a, cq * a.Hq + g * G + h, d, D, M, Ls, O);

@@ -117,7 +117,6 @@ constexpr int kRowBlock = 64;              // rows of the f32 merge staging
 constexpr int kMinChunk = 256;             // a default chunk is at least this long
 constexpr int kMaxChunks = 32;             // default chunks per part (prompt, generated)
 constexpr int kMaxSlots = 64;              // partial results per (cell, KV head)
-constexpr int kGenStage = 4096;            // bf16: (m, l) pairs x chunks x heads a generated item stages
 constexpr int kPromptItemsTarget = 512;    // f32 prompt items a default split aims for
 constexpr int kGenItemsTarget = 2048;      // f32 generated items a default split aims for
 constexpr int kWideItemsTarget = 512;      // bf16 prompt work groups a default split aims for
@@ -217,15 +216,12 @@ struct AttnPlan {
 // consecutive cells of one KV head, NW / P waves each.  Each wave should
 // stream at least two 16-row tiles, so short generated parts pack many
 // cells into a work group and long ones spread one cell over all waves.
-// The staging of the pairs' prompt (m, l) bounds P.
-inline int gen_pairs(const splice_shape &sh, int n_gen, int n_p) {
+inline int gen_pairs(const splice_shape &sh, int n_gen) {
     const int nw = fused_waves(sh.head_dim);
     const int tiles = ceil_div(n_gen, 16);
     int wpp = nw;
     while (wpp > 1 && tiles < 2 * wpp) wpp /= 2;
-    int P = nw / wpp;
-    while (P > 1 && P * n_p * group_of(sh) > kGenStage) P /= 2;
-    return P;
+    return nw / wpp;
 }
 
 // Cells of the call that are not spliced.
@@ -264,7 +260,7 @@ inline AttnPlan plan_attn(const splice_shape &sh, const splice_call &call, int n
         p.n_prompt_items = prompt_items_per_chunk(sh, n_clean) * p.n_p;
     }
     if (bf16_path(sh)) {
-        p.gen_pairs = gen_pairs(sh, p.geo.n_gen, p.n_p);
+        p.gen_pairs = gen_pairs(sh, p.geo.n_gen);
         p.n_gen_items = ceil_div(sh.n_cells, p.gen_pairs) * sh.n_kv_heads;
     } else {
         p.gen_pairs = 1;
