@@ -26,6 +26,7 @@ struct AttnArgs {
     int n_rg_clean;   // bf16 prompt row groups of unspliced cells (the rest: spliced cells)
     int wait_polls;   // bf16 generated-row items: most polls for the prompt partials
     int gen_pairs;    // bf16 generated-row items: (cell, KV head) pairs per work group
+    int gen_v_nt;     // bf16 generated-row items: V rows loaded non-temporally
     float qk_scale;   // scale * log2(e)
     uint32_t spliced[SPLICE_MAX_CELLS / 32];
     uint8_t order[SPLICE_MAX_CELLS];   // clean cells, then spliced cells
@@ -471,12 +472,15 @@ __device__ void combine_cells(const AttnArgs &a, const int *list, int n, int g, 
                            __HIP_MEMORY_SCOPE_AGENT);
 }
 
-// Cache policy of row loads: normal.  Each K load instruction covers 64
-// bytes of 16 rows (the MFMA operand layout), so the other half of every
-// 128-byte line arrives with the next instruction; non-temporal loads, which
-// do not keep the line, measured slower here.
-constexpr int kLoadCached = 0;
-constexpr int kGenAux = kLoadCached;
+// Cache policies of the generated-row loads.  Each K load instruction covers
+// 64 bytes of 16 rows (the MFMA operand layout), so the other half of every
+// 128-byte line arrives with the next instruction: K loads stay normal
+// (non-temporal ones, which do not keep the line, measured slower).  V
+// loads cover whole lines; with a long prompt they are non-temporal, so that
+// the generated rows, read once, do not push the prompt tiles the prompt
+// items share out of the caches (the host sets AttnArgs::gen_v_nt).
+constexpr int kAuxNormal = 0;
+constexpr int kAuxStream = 2;
 
 // f32 inputs, one launch per call: blocks [0, n_prompt_items) are prompt
 // items (cell, KV head, prompt chunk), the rest generated-row items; the
@@ -693,7 +697,12 @@ __device__ int fused_gen_item(const AttnArgs &a, int item, char *lds, int *s_lis
     WaveState<D> S;
     state_init(S);
     const ColMask cm{true, true, true};
-    wave_stream<D, Fused<D>::GEN_DEPTH, kGenAux>(L, wave % wpp, wpp, cm, qb, a.qk_scale, lds + wave * W::LDS, S);
+    if (a.gen_v_nt)
+        wave_stream<D, Fused<D>::GEN_DEPTH, kAuxNormal, kAuxStream>(L, wave % wpp, wpp, cm, qb, a.qk_scale,
+                                                                     lds + wave * W::LDS, S);
+    else
+        wave_stream<D, Fused<D>::GEN_DEPTH, kAuxNormal, kAuxNormal>(L, wave % wpp, wpp, cm, qb, a.qk_scale,
+                                                                     lds + wave * W::LDS, S);
     state_finish(S);
 
     if (threadIdx.x == 0) {

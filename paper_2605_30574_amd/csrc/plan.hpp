@@ -269,6 +269,18 @@ inline AttnPlan plan_attn(const splice_shape &sh, const splice_call &call, int n
     return p;
 }
 
+// bf16: the generated-row items load V non-temporally when the prompt
+// caches a call reads (clean, plus donor when the donor is a buffer) exceed
+// this many bytes; below it the prompt stays cached either way and normal
+// loads measured faster.
+constexpr int64_t kGenNtPromptBytes = (int64_t)16 << 20;
+
+inline bool gen_v_nontemporal(const splice_shape &sh) {
+    const int64_t per_cache = (int64_t)sh.prompt_len * sh.n_kv_heads * sh.head_dim * elem_bytes(sh) * 2;
+    const int64_t bytes = per_cache * (sh.donor_kind == SPLICE_DONOR_BUFFER ? 2 : 1);
+    return bytes > kGenNtPromptBytes;
+}
+
 struct WorkspaceLayout {
     size_t counters_off, counters_bytes;
     size_t part_off, part_bytes;

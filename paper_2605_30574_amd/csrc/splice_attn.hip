@@ -282,6 +282,7 @@ int32_t splice_decode_attn(const splice_shape *shape, const splice_call *call, c
     a.n_rg_clean = splice::bf16_path(sh) ? splice::clean_row_groups(sh, n_clean) : 0;
     a.n_prompt_items = plan.n_prompt_items;
     a.gen_pairs = plan.gen_pairs;
+    a.gen_v_nt = splice::gen_v_nontemporal(sh) ? 1 : 0;
     a.wait_polls = call->merge_wait == 0 ? kDefaultWaitPolls : (call->merge_wait < 0 ? 0 : call->merge_wait);
     a.qk_scale = call->scale * kLog2e;
     fill_mask(sh, *call, cell_LW, a.spliced);

@@ -159,19 +159,19 @@ __device__ __forceinline__ u32x4_t row_load(__amdgpu_buffer_rsrc_t r, int off) {
     return __builtin_bit_cast(u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, AUX));
 }
 
-template <int D, int AUX>
+template <int D, int KAUX, int VAUX>
 __device__ __forceinline__ void tile_load_aux(const TileRef &t, TileRegs<D> &r) {
     using W = WaveMfma<D>;
     const int lane = threadIdx.x & 63, col = lane & 15, quad = lane >> 4;
     const __amdgpu_buffer_rsrc_t rk = rows_rsrc(t.k, t.n * W::ROW);
     const __amdgpu_buffer_rsrc_t rv = rows_rsrc(t.v, t.n * W::ROW);
     const int koff = col * W::ROW + 16 * quad;
-    static_for<0, W::NDS>([&](auto st) { r.k[st] = row_load<AUX>(rk, koff + 64 * st); });
+    static_for<0, W::NDS>([&](auto st) { r.k[st] = row_load<KAUX>(rk, koff + 64 * st); });
     static_for<0, W::NVU>([&](auto n) {
         const int u = lane + 64 * n;
         const int kq = u & 3, dg = u >> 2;   // unit: keys 4 kq .. 4 kq + 3, bytes 16 dg .. 16 dg + 15
         if (u < W::UNITS) {
-            static_for<0, 4>([&](auto kk) { r.v[n][kk] = row_load<AUX>(rv, (4 * kq + kk) * W::ROW + 16 * dg); });
+            static_for<0, 4>([&](auto kk) { r.v[n][kk] = row_load<VAUX>(rv, (4 * kq + kk) * W::ROW + 16 * dg); });
         }
     });
 }
@@ -286,10 +286,11 @@ __device__ __forceinline__ void tile_compute(const u32x4_t (&kr)[WaveMfma<D>::ND
 // Stream tiles t = first, first + step, ... of the list through one wave,
 // keeping DEPTH tiles in flight: when tile t is computed, the loads of the
 // next DEPTH - 1 tiles are outstanding.  The loop is unrolled DEPTH times so
-// the register sets are only ever indexed by constants.  AUX is the cache
-// policy of every row load (0 normal, 2 non-temporal); it is a constant so
-// that every path issues the same loads.
-template <int D, int DEPTH, int AUX>
+// the register sets are only ever indexed by constants.  KAUX and VAUX are
+// the cache policies of the K and the V row loads (0 normal, 2
+// non-temporal); they are constants so that every path issues the same
+// loads.
+template <int D, int DEPTH, int KAUX, int VAUX>
 __device__ __forceinline__ void wave_stream(const KeyList &L, int first, int step, const ColMask &cm,
                                             const bf16x8_t (&qb)[WaveMfma<D>::NDS], float qk_scale, char *sVt,
                                             WaveState<D> &S) {
@@ -299,7 +300,7 @@ __device__ __forceinline__ void wave_stream(const KeyList &L, int first, int ste
     TileRef ref[DEPTH];
     static_for<0, DEPTH>([&](auto i) {
         ref[i] = list_tile_or_empty(L, first + i * step, n_tiles, WaveMfma<D>::ROW);
-        tile_load_aux<D, AUX>(ref[i], r[i]);
+        tile_load_aux<D, KAUX, VAUX>(ref[i], r[i]);
     });
     for (int base = first; base < n_tiles; base += DEPTH * step) {
         static_for<0, DEPTH>([&](auto j) {
@@ -314,7 +315,7 @@ __device__ __forceinline__ void wave_stream(const KeyList &L, int first, int ste
             static_for<0, WaveMfma<D>::NDS>([&](auto st) { kr[st] = r[j].k[st]; });
             const TileRef cur = ref[j];
             ref[j] = list_tile_or_empty(L, t + DEPTH * step, n_tiles, WaveMfma<D>::ROW);
-            tile_load_aux<D, AUX>(ref[j], r[j]);
+            tile_load_aux<D, KAUX, VAUX>(ref[j], r[j]);
             if (live) tile_compute<D>(kr, cur.n, cm.on(cur.cols), qb, qk_scale, sVt, S);
         });
     }
