@@ -556,7 +556,7 @@ struct Fused {
 };
 
 // Prompt slots a generated-row item loads in one round for its merge.
-constexpr int kMergeBatch = 8;
+constexpr int kMergeBatch = 16;
 
 template <int D, int G>
 struct FusedLds {

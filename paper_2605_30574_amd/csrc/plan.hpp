@@ -164,11 +164,16 @@ inline int prompt_items_bound(const splice_shape &sh) {
     return sh.n_kv_heads * (ceil_div((int64_t)sh.n_cells * group_of(sh), group_rows(sh.head_dim)) + 1);
 }
 
+// bf16: at most this many prompt chunks by default, so that a generated-row
+// item merges every prompt slot in one round of loads.
+constexpr int kWideMaxChunks = 16;
+
 inline int prompt_chunk_target(const splice_shape &sh) {
     const int per = prompt_items_bound(sh);
     const int want = bf16_path(sh) ? kWideItemsTarget : kPromptItemsTarget;
+    const int cap = bf16_path(sh) ? kWideMaxChunks : kMaxChunks;
     const int t = per > 0 ? want / per : 1;
-    return t < 1 ? 1 : (t > kMaxChunks ? kMaxChunks : t);
+    return t < 1 ? 1 : (t > cap ? cap : t);
 }
 
 inline int gen_chunk_target(const splice_shape &sh) {
