@@ -555,8 +555,34 @@ struct Fused {
     static_assert(ROWS == NW * 16 * RB, "host and device agree on the row groups");
 };
 
-// Prompt slots a generated-row item loads in one round for its merge.
-constexpr int kMergeBatch = 16;
+// The prompt slots 0 .. n_p - 1 (n_p <= B) of one (row, four outputs) in one
+// round of loads: M over the slots and this item's own maximum Mg, the ZERO
+// term, then the slots folded in order (the fixed fold order).
+template <int B>
+__device__ __forceinline__ void merge_slots_once(const AttnArgs &a, __amdgpu_buffer_rsrc_t r, uint32_t sbase,
+                                                 uint32_t slot_bytes, uint32_t o_off, uint32_t m_off,
+                                                 uint32_t l_off, bool zero_term, float Mg, float &M, float &Ls,
+                                                 f32x4_t &O) {
+    f32x4_t ok[B];
+    float mk[B], lk[B];
+#pragma unroll
+    for (int j = 0; j < B; ++j) {
+        if (j < a.n_p) {
+            const uint32_t off = sbase + (uint32_t)j * slot_bytes;
+            ok[j] = part_load4(r, off + o_off);
+            mk[j] = part_load1(r, off + m_off);
+            lk[j] = part_load1(r, off + l_off);
+        }
+    }
+#pragma unroll
+    for (int j = 0; j < B; ++j)
+        if (j < a.n_p) M = fmaxf(M, mk[j]);
+    M = fmaxf(M, Mg);
+    if (zero_term) Ls = (float)(a.sb - a.sa) * fast_exp2(-M);
+#pragma unroll
+    for (int j = 0; j < B; ++j)
+        if (j < a.n_p) fold_slot(mk[j], lk[j], ok[j], M, Ls, O);
+}
 
 template <int D, int G>
 struct FusedLds {
@@ -736,29 +762,12 @@ __device__ int fused_gen_item(const AttnArgs &a, int item, char *lds, int *s_lis
             float M = zero_term ? 0.f : -INFINITY;
             float Ls = 0.f;
             f32x4_t O = {0.f, 0.f, 0.f, 0.f};
-            constexpr int B = kMergeBatch;
-            if (a.n_p <= B) {
-                // one round of loads: every prompt slot's (m, l, o) at once
-                f32x4_t ok[B];
-                float mk[B], lk[B];
-#pragma unroll
-                for (int j = 0; j < B; ++j) {
-                    const uint32_t off = sbase + (uint32_t)min(j, max(a.n_p - 1, 0)) * slot_bytes;
-                    if (j < a.n_p) {
-                        ok[j] = part_load4(r, off + o_off);
-                        mk[j] = part_load1(r, off + m_off);
-                        lk[j] = part_load1(r, off + l_off);
-                    }
-                }
-#pragma unroll
-                for (int j = 0; j < B; ++j)
-                    if (j < a.n_p) M = fmaxf(M, mk[j]);
-                M = fmaxf(M, Mg);
-                if (zero_term) Ls = (float)(a.sb - a.sa) * fast_exp2(-M);
-#pragma unroll
-                for (int j = 0; j < B; ++j)
-                    if (j < a.n_p) fold_slot(mk[j], lk[j], ok[j], M, Ls, O);
+            if (a.n_p <= 8) {
+                merge_slots_once<8>(a, r, sbase, slot_bytes, o_off, m_off, l_off, zero_term, Mg, M, Ls, O);
+            } else if (a.n_p <= 16) {
+                merge_slots_once<16>(a, r, sbase, slot_bytes, o_off, m_off, l_off, zero_term, Mg, M, Ls, O);
             } else {
+                constexpr int B = 8;
                 for (int k = 0; k < a.n_p; ++k) M = fmaxf(M, part_load1(r, sbase + (uint32_t)k * slot_bytes + m_off));
                 M = fmaxf(M, Mg);
                 if (zero_term) Ls = (float)(a.sb - a.sa) * fast_exp2(-M);

@@ -358,14 +358,20 @@ __device__ __forceinline__ void waves_merge(WaveState<D> &S, char *buf, int wpp,
         const int p = e / UPG, h = (e % UPG) / (D / 4), d = 4 * (e % (D / 4));
         const int w0 = p * wpp;
         float M = -INFINITY;
-        for (int w = w0; w < w0 + wpp; ++w) M = fmaxf(M, s_m[w * G + h]);
+#pragma unroll
+        for (int i = 0; i < NW; ++i)
+            if (i < wpp) M = fmaxf(M, s_m[(w0 + i) * G + h]);
         const float Ms = M == -INFINITY ? 0.f : M;
         float L = 0.f;
         f32x4_t O = {0.f, 0.f, 0.f, 0.f};
-        for (int w = w0; w < w0 + wpp; ++w) {
-            const float f = fast_exp2(s_m[w * G + h] - Ms);
-            L = fmaf(s_l[w * G + h], f, L);
-            O += *reinterpret_cast<const f32x4_t *>(s_o + (w * G + h) * D + d) * f;
+#pragma unroll
+        for (int i = 0; i < NW; ++i) {
+            if (i < wpp) {
+                const int w = w0 + i;
+                const float f = fast_exp2(s_m[w * G + h] - Ms);
+                L = fmaf(s_l[w * G + h], f, L);
+                O += *reinterpret_cast<const f32x4_t *>(s_o + (w * G + h) * D + d) * f;
+            }
         }
         sink(p, h, d, M, L, O);
     }
