@@ -14,6 +14,8 @@ Reported (one JSON line):
               it, donor span if a spliced cell reads a donor buffer, every
               cell's visible generated rows, out and lse);
   cell_steps_per_s   C * K / wall time;
+  per_step    time per launch and GB/s of one step's N launches at
+              s = 0, S/4, S/2, S - 1 (measured after the timed region);
   roofline    bound "hbm": achieved = algorithmic bytes per call / average
               call duration (HIP events on the launch stream, over the timed
               region; a call is one kernel launch), peak 8000 GB/s,
@@ -209,6 +211,7 @@ def main():
     K = args.steps if args.steps > 0 else S
     timed_steps = [min(S - 1, int((i + 0.5) * S / K)) for i in range(K)]
     warm_steps = [min(S - 1, int((i + 0.5) * S / max(1, args.warmup))) for i in range(args.warmup)]
+    bucket_steps = sorted({0, S // 4, S // 2, S - 1})
 
     log(f"workload {w.name}: N={N} C={C} Hq={w.n_q_heads} Hkv={w.n_kv_heads} D={w.head_dim} "
         f"T_p={w.prompt_len} S={S}; timed steps K={K}")
@@ -237,7 +240,7 @@ def main():
     graphs = {}
     if not args.eager:
         t0 = time.time()
-        for s in sorted(set(timed_steps) | set(warm_steps)):
+        for s in sorted(set(timed_steps) | set(warm_steps) | set(bucket_steps)):
             g = torch.cuda.CUDAGraph()
             with torch.cuda.graph(g, stream=stream):
                 issue_step(s)
@@ -270,6 +273,25 @@ def main():
     log(f"timed {launches} launches in {ms:.2f} ms: {gbs:.1f} GB/s algorithmic, "
         f"{C * K / sec:.0f} cell-steps/s")
 
+    # per-step buckets (outside the timed region): one step's N launches,
+    # replayed a few times, at s = 0, S/4, S/2, S - 1
+    per_step = {}
+    for s in bucket_steps:
+        reps = 5
+        run([s])
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record(stream)
+        run([s] * reps)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        t = e0.elapsed_time(e1) / 1e3 / reps
+        b = sum(call_bytes(w, l, s, spliced_flags(w, l, s)) for l in range(N))
+        per_step[str(s)] = {"us_per_launch": round(t / N * 1e6, 2), "GB/s": round(b / t / 1e9, 1)}
+    log("per-step buckets: " + ", ".join(f"s={k}: {v['us_per_launch']} us/launch, {v['GB/s']} GB/s"
+                                          for k, v in per_step.items()))
+
     traffic, traffic_src = stored_traffic(w.name)
     per_launch_bytes = alg_bytes / launches
     avg_launch_s = sec / launches
@@ -301,6 +323,7 @@ def main():
                    "timed_steps": "evenly spaced over the sweep" if K != S else "full sweep"},
         "roofline": roofline,
         "cpu_baseline": cpu,
+        "per_step": per_step,
     }
     print(json.dumps(res), flush=True)
 
