@@ -58,7 +58,7 @@ extern "C" {
 #define SPLICE_API
 #endif
 
-#define SPLICE_ABI_VERSION 2
+#define SPLICE_ABI_VERSION 3
 #define SPLICE_MAX_CELLS 256
 
 typedef enum {
@@ -143,9 +143,10 @@ SPLICE_API int64_t splice_decode_attn_workspace_bytes(const splice_shape *shape,
 
 /*
  * Zero a workspace with a fill kernel enqueued on `stream` (no memset node,
- * so it may be graph-captured).  splice_decode_attn does not depend on the
- * workspace's prior contents -- it writes every partial-result slot before a
- * second kernel of the same call reads it -- so this is optional hygiene.
+ * so it may be graph-captured).  Required once before a workspace's first
+ * splice_decode_attn / splice_decode_step: the workspace starts with the
+ * per-(cell, KV head) arrival counters, which must start at zero; every call
+ * re-arms the counters it used, so later calls need no re-initialisation.
  * workspace must be 256-byte aligned and workspace_bytes a multiple of 4.
  */
 SPLICE_API int32_t splice_workspace_init(void *workspace, size_t workspace_bytes, void *stream);
@@ -157,9 +158,9 @@ SPLICE_API int32_t splice_workspace_init(void *workspace, size_t workspace_bytes
  *   out     = softmax(score) . V,     lse = log sum_j exp(score_j),
  * with the keys and values chosen per cell as described at the top.
  * q is read in dtype; accumulation is fp32; out and lse are fp32.
- * `workspace` (256-byte aligned) must hold
- * splice_decode_attn_workspace_bytes(shape, call) bytes; it holds the
- * split-K partial results between the call's two kernels, so calls that
+ * `workspace` (256-byte aligned, initialised once by splice_workspace_init)
+ * must hold splice_decode_attn_workspace_bytes(shape, call) bytes; it holds
+ * the split-K partial results and arrival counters of a call, so calls that
  * share a workspace must be ordered on one stream.
  */
 SPLICE_API int32_t splice_decode_attn(const splice_shape *shape, const splice_call *call,
@@ -168,6 +169,42 @@ SPLICE_API int32_t splice_decode_attn(const splice_shape *shape, const splice_ca
                            const void *clean_k, const void *clean_v,
                            const void *donor_k, const void *donor_v,
                            const void *gen_k, const void *gen_v,
+                           float *out, float *lse,
+                           void *workspace, size_t workspace_bytes,
+                           void *stream);
+
+/*
+ * One decode pass of a batch of cells, each at its own step (Algorithm 1:
+ * the forward pass appends the current token's K/V to the generated cache,
+ * then attends; a trajectory stops at EOS).  cell_step is host int32 [C]:
+ *   cell_step[c] = s_c >= 0  active cell at 0-based step s_c <
+ *                            shape->gen_capacity: row s_c of its generated
+ *                            caches gen_k, gen_v ([C][Hkv][cap][D]) is set to
+ *                            k_new[c], v_new[c] ([C][Hkv][D], dtype), then
+ *                            out[c], lse[c] are computed exactly as
+ *                            splice_decode_attn at call->step = s_c (the
+ *                            splice predicate uses s_c; a sliding window ends
+ *                            at T_p + s_c);
+ *   cell_step[c] < 0         finished cell (EOS): nothing read or written.
+ * call->step is ignored (the other fields of call are validated as usual).
+ * The workspace must hold splice_decode_attn_workspace_bytes(shape, NULL)
+ * bytes, or with an explicit split_keys, splice_decode_attn_workspace_bytes
+ * (shape, call') with call'->step the smallest s_c (the step that sees the
+ * most prompt slots).  Only rows s_c of active cells' generated caches are
+ * written; the attention of the call takes row s_c from k_new, v_new, so it
+ * never depends on when the write lands.  A call with every cell finished is
+ * a valid no-op.
+ * Errors: as splice_decode_attn, plus SPLICE_EINVAL for a NULL cell_step,
+ * k_new or v_new, SPLICE_ESHAPE for s_c >= gen_capacity, and
+ * SPLICE_EUNSUPPORTED for f32 inputs (bf16 only).  Other conventions as
+ * splice_decode_attn.
+ */
+SPLICE_API int32_t splice_decode_step(const splice_shape *shape, const splice_call *call,
+                           const int32_t *cell_LW, const int32_t *cell_step,
+                           const void *q, const void *k_new, const void *v_new,
+                           const void *clean_k, const void *clean_v,
+                           const void *donor_k, const void *donor_v,
+                           void *gen_k, void *gen_v,
                            float *out, float *lse,
                            void *workspace, size_t workspace_bytes,
                            void *stream);

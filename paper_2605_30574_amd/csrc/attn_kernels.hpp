@@ -25,6 +25,13 @@ struct AttnArgs {
     int n_rb, n_prompt_items, n_clean;
     int n_rg_clean;   // bf16 prompt row groups of unspliced cells (the rest: spliced cells)
     int wait_polls;   // bf16 generated-row items: most polls for the prompt partials
+    int n_active;     // cells in `order` (all cells, or the unfinished ones of a decode step)
+    int ragged;       // bf16: each cell at its own step cstep[c] (< 0: finished, skipped)
+    int window;       // sliding window of the call (0: every key visible)
+    int span_lo, span_hi;
+    int row_lo;       // prompt items mask the keys before each row's first visible slot
+    const char *kn, *vn;   // bf16 decode step: the current token's K, V [C][Hkv][D], appended
+    int32_t cstep[SPLICE_MAX_CELLS];
     int gen_pairs;    // bf16 generated-row items: (cell, KV head) pairs per work group
     int gen_v_nt;     // bf16 generated-row items: V rows loaded non-temporally
     float qk_scale;   // scale * log2(e)
@@ -384,9 +391,35 @@ __device__ __forceinline__ void fold_slot(float mk, float lk, f32x4_t ok, float 
     O.w = fmaf(ok.w, f, O.w);
 }
 
-__device__ __forceinline__ bool has_zero_term(const AttnArgs &a, int c) {
-    return a.zero_donor && bit_set(a.spliced, c) && a.sb > a.sa;
+// What cell c sees: its step, visible generated rows [i0, i0 + n_gen), first
+// visible prompt slot jp0 and visible span [sa, sb) -- the call's values, or
+// the cell's own under a decode step with cells at different steps.
+struct CellGeo {
+    int s, i0, n_gen, jp0, sa, sb;
+};
+
+__device__ __forceinline__ CellGeo cell_geo(const AttnArgs &a, int c) {
+    if (!a.ragged) return CellGeo{a.i0 + a.n_gen - 1, a.i0, a.n_gen, a.jp0, a.sa, a.sb};
+    const int s = a.cstep[c];
+    const int j0 = a.window > 0 ? a.Tp + s - a.window + 1 : 0;
+    const int jp0 = min(max(j0, 0), a.Tp);
+    const int i0 = max(j0 - a.Tp, 0);
+    const int sa = min(max(a.span_lo, jp0), a.Tp);
+    const int sb = min(max(a.span_hi, sa), a.Tp);
+    return CellGeo{s, i0, s + 1 - i0, jp0, sa, sb};
 }
+
+__device__ __forceinline__ bool cell_active(const AttnArgs &a, int c) { return !a.ragged || a.cstep[c] >= 0; }
+
+// ZERO-donor slots cell c sees (0 without a ZERO term): keys of score 0 and
+// value 0, added in closed form by the merge.
+__device__ __forceinline__ int zero_slots(const AttnArgs &a, int c) {
+    if (!a.zero_donor || !bit_set(a.spliced, c)) return 0;
+    const CellGeo geo = cell_geo(a, c);
+    return geo.sb - geo.sa;
+}
+
+__device__ __forceinline__ bool has_zero_term(const AttnArgs &a, int c) { return zero_slots(a, c) > 0; }
 
 __device__ __forceinline__ void write_row(const AttnArgs &a, int row, int d, int D, float M, float L, f32x4_t O) {
     *reinterpret_cast<f32x4_t *>(a.out + (size_t)row * D + d) = O * (1.f / L);
@@ -432,7 +465,7 @@ __device__ void combine_cells(const AttnArgs &a, const int *list, int n, int g, 
             float mx = zero_term ? 0.f : -INFINITY;
             for (int k = 0; k < a.n_slots; ++k) mx = fmaxf(mx, s_m[sm_off[b] + k * G]);
             M[b] = mx;
-            L[b] = zero_term ? (float)(a.sb - a.sa) * fast_exp2(-mx) : 0.f;
+            L[b] = zero_term ? (float)zero_slots(a, c) * fast_exp2(-mx) : 0.f;
             O[b] = f32x4_t{0.f, 0.f, 0.f, 0.f};
         }
         int k = 0;
@@ -561,7 +594,7 @@ struct Fused {
 template <int B>
 __device__ __forceinline__ void merge_slots_once(const AttnArgs &a, __amdgpu_buffer_rsrc_t r, uint32_t sbase,
                                                  uint32_t slot_bytes, uint32_t o_off, uint32_t m_off,
-                                                 uint32_t l_off, bool zero_term, float Mg, float &M, float &Ls,
+                                                 uint32_t l_off, int nz, float Mg, float &M, float &Ls,
                                                  f32x4_t &O) {
     f32x4_t ok[B];
     float mk[B], lk[B];
@@ -578,7 +611,7 @@ __device__ __forceinline__ void merge_slots_once(const AttnArgs &a, __amdgpu_buf
     for (int j = 0; j < B; ++j)
         if (j < a.n_p) M = fmaxf(M, mk[j]);
     M = fmaxf(M, Mg);
-    if (zero_term) Ls = (float)(a.sb - a.sa) * fast_exp2(-M);
+    if (nz > 0) Ls = (float)nz * fast_exp2(-M);
 #pragma unroll
     for (int j = 0; j < B; ++j)
         if (j < a.n_p) fold_slot(mk[j], lk[j], ok[j], M, Ls, O);
@@ -619,12 +652,12 @@ __device__ int fused_prompt_item(const AttnArgs &a, int item, char *lds, int *s_
     const int lane = threadIdx.x & 63, col = lane & 15, quad = lane >> 4;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     bf16x8_t qb[RB][X::NDS];
-    int cell[RB], hh[RB];
+    int cell[RB], hh[RB], lo[RB];
     bool ok[RB];
     // row groups of unspliced cells come first; a group never mixes classes
     const bool clean_group = rg < a.n_rg_clean;
     const int first_cell = clean_group ? 0 : a.n_clean;
-    const int end_cell = clean_group ? a.n_clean : a.C;
+    const int end_cell = clean_group ? a.n_clean : a.n_active;
     const int grp = clean_group ? rg : rg - a.n_rg_clean;
     static_for<0, RB>([&](auto rb) {
         const int R = grp * ROWS + (wave * RB + rb) * 16 + col;
@@ -632,6 +665,7 @@ __device__ int fused_prompt_item(const AttnArgs &a, int item, char *lds, int *s_
         ok[rb] = cidx < end_cell;
         cell[rb] = ok[rb] ? a.order[cidx] : 0;
         hh[rb] = R % G;
+        lo[rb] = a.row_lo && ok[rb] ? cell_geo(a, cell[rb]).jp0 : 0;
         load_q_cols<D>(ok[rb] ? a.q + ((size_t)cell[rb] * a.Hq + (size_t)g * G + hh[rb]) * X::ROW : nullptr,
                        qb[rb]);
     });
@@ -646,14 +680,14 @@ __device__ int fused_prompt_item(const AttnArgs &a, int item, char *lds, int *s_
     const int pre1 = min(k1, a.sa), sp0 = max(k0, a.sa), sp1 = min(k1, a.sb), post0 = max(k0, a.sb);
     KeyList L;
     list_init(L);
-    list_add<X::TK>(L, ck + (size_t)k0 * X::ROW, cv + (size_t)k0 * X::ROW, pre1 - k0);
+    list_add<X::TK>(L, ck + (size_t)k0 * X::ROW, cv + (size_t)k0 * X::ROW, pre1 - k0, kColsAll, k0);
     if (clean_group) {
-        list_add<X::TK>(L, ck + (size_t)sp0 * X::ROW, cv + (size_t)sp0 * X::ROW, sp1 - sp0);
+        list_add<X::TK>(L, ck + (size_t)sp0 * X::ROW, cv + (size_t)sp0 * X::ROW, sp1 - sp0, kColsAll, sp0);
     } else if (!a.zero_donor) {
         const char *dk = a.dk + head, *dv = a.dv + head;
-        list_add<X::TK>(L, dk + (size_t)sp0 * X::ROW, dv + (size_t)sp0 * X::ROW, sp1 - sp0);
+        list_add<X::TK>(L, dk + (size_t)sp0 * X::ROW, dv + (size_t)sp0 * X::ROW, sp1 - sp0, kColsAll, sp0);
     }
-    list_add<X::TK>(L, ck + (size_t)post0 * X::ROW, cv + (size_t)post0 * X::ROW, k1 - post0);
+    list_add<X::TK>(L, ck + (size_t)post0 * X::ROW, cv + (size_t)post0 * X::ROW, k1 - post0, kColsAll, post0);
 
     WideState<D, RB> S;
     static_for<0, RB>([&](auto rb) {
@@ -661,7 +695,7 @@ __device__ int fused_prompt_item(const AttnArgs &a, int item, char *lds, int *s_
         S.m[rb] = -INFINITY;
         S.lsum[rb] = 0.f;
     });
-    wide_stream<D, RB, Fused<D>::PROMPT_DEPTH, Fused<D>::NT>(L, qb, a.qk_scale, lds, S);
+    wide_stream<D, RB, Fused<D>::PROMPT_DEPTH, Fused<D>::NT>(L, qb, a.qk_scale, a.row_lo != 0, lo, lds, S);
 
     const __amdgpu_buffer_rsrc_t r = part_rsrc(a);
     static_for<0, RB>([&](auto rb) {
@@ -699,26 +733,46 @@ __device__ int fused_prompt_item(const AttnArgs &a, int item, char *lds, int *s_
 // dispatched first and finish).  Then this item merges in place: its own
 // partial is the last slot and never leaves the chip.  Past the bound it
 // stores its partials and counts itself like any other item, and the last
-// arrival merges.
+// arrival merges.  Under a decode step the item first appends each active
+// cell's new row (a.kn, a.vn) to its generated caches, and streams that row
+// from a.kn, a.vn rather than reading it back; finished cells are skipped.
 template <int D, int G>
 __device__ int fused_gen_item(const AttnArgs &a, int item, char *lds, int *s_list) {
     using W = WaveMfma<D>;
-    constexpr int NW = Fused<D>::NW;
+    constexpr int NW = Fused<D>::NW, NT = Fused<D>::NT;
     const int P = a.gen_pairs, wpp = NW / P;
     const int g = item % a.Hkv;
     const int c0 = (item / a.Hkv) * P;
     const int n_pairs = min(P, a.C - c0);
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int c = c0 + wave / wpp;   // this wave's cell
-    const bool valid = c < a.C;
+    const bool valid = c < a.C && cell_active(a, c);
     const int col = threadIdx.x & 15;
+    if (a.kn) {   // append: row s of each active cell's generated K and V
+        constexpr int U = W::ROW / 16;   // 16-byte units of a row
+        for (int t = threadIdx.x; t < n_pairs * 2 * U; t += NT) {
+            const int cq = c0 + t / (2 * U), kv = (t / U) & 1, u = t % U;
+            if (!cell_active(a, cq)) continue;
+            const size_t src = ((size_t)cq * a.Hkv + g) * W::ROW + 16 * u;
+            const size_t dst = (((size_t)cq * a.Hkv + g) * (size_t)a.cap + cell_geo(a, cq).s) * W::ROW + 16 * u;
+            char *to = const_cast<char *>(kv ? a.gv : a.gk);
+            *reinterpret_cast<u32x4_t *>(to + dst) = *reinterpret_cast<const u32x4_t *>((kv ? a.vn : a.kn) + src);
+        }
+    }
     bf16x8_t qb[W::NDS];
     load_q_cols<D>(valid ? a.q + ((size_t)c * a.Hq + (size_t)g * G + col % G) * W::ROW : nullptr, qb);
     KeyList L;
     list_init(L);
     if (valid) {
-        const size_t goff = (((size_t)c * a.Hkv + g) * (size_t)a.cap + a.i0) * W::ROW;
-        list_add(L, a.gk + goff, a.gv + goff, a.n_gen);
+        const CellGeo geo = cell_geo(a, c);
+        const size_t goff = (((size_t)c * a.Hkv + g) * (size_t)a.cap + geo.i0) * W::ROW;
+        if (a.kn) {   // rows before the current one from the cache, the current one as given
+            list_add(L, a.gk + goff, a.gv + goff, geo.n_gen - 1);
+            const size_t noff = ((size_t)c * a.Hkv + g) * W::ROW;
+            list_add(L, a.kn + noff, a.vn + noff, 1);
+        } else {
+            list_add(L, a.gk + goff, a.gv + goff, geo.n_gen);
+        }
     }
     WaveState<D> S;
     state_init(S);
@@ -735,6 +789,7 @@ __device__ int fused_gen_item(const AttnArgs &a, int item, char *lds, int *s_lis
         bool ready = true;
         int polls = 0;
         for (int q = 0; q < n_pairs && ready; ++q) {
+            if (!cell_active(a, c0 + q)) continue;
             const int *cnt = a.counters + (c0 + q) * a.Hkv + g;
             bool done = a.n_p == 0;
             while (!done && polls < a.wait_polls) {
@@ -755,22 +810,23 @@ __device__ int fused_gen_item(const AttnArgs &a, int item, char *lds, int *s_lis
     if (ready) {
         waves_merge<D, G, NW>(S, lds, wpp, n_pairs, [&](int q, int h, int d, float Mg, float Lg, f32x4_t Og) {
             const int cq = c0 + q;
+            if (!cell_active(a, cq)) return;
             const uint32_t sbase = slot_off(a, cq, g, 0);
             const uint32_t o_off = (uint32_t)(h * D + d) * 4u;
             const uint32_t m_off = (uint32_t)(G * D + h) * 4u, l_off = (uint32_t)(G * D + G + h) * 4u;
-            const bool zero_term = has_zero_term(a, cq);
-            float M = zero_term ? 0.f : -INFINITY;
+            const int nz = zero_slots(a, cq);
+            float M = nz > 0 ? 0.f : -INFINITY;
             float Ls = 0.f;
             f32x4_t O = {0.f, 0.f, 0.f, 0.f};
             if (a.n_p <= 8) {
-                merge_slots_once<8>(a, r, sbase, slot_bytes, o_off, m_off, l_off, zero_term, Mg, M, Ls, O);
+                merge_slots_once<8>(a, r, sbase, slot_bytes, o_off, m_off, l_off, nz, Mg, M, Ls, O);
             } else if (a.n_p <= 16) {
-                merge_slots_once<16>(a, r, sbase, slot_bytes, o_off, m_off, l_off, zero_term, Mg, M, Ls, O);
+                merge_slots_once<16>(a, r, sbase, slot_bytes, o_off, m_off, l_off, nz, Mg, M, Ls, O);
             } else {
                 constexpr int B = 8;
                 for (int k = 0; k < a.n_p; ++k) M = fmaxf(M, part_load1(r, sbase + (uint32_t)k * slot_bytes + m_off));
                 M = fmaxf(M, Mg);
-                if (zero_term) Ls = (float)(a.sb - a.sa) * fast_exp2(-M);
+                if (nz > 0) Ls = (float)nz * fast_exp2(-M);
                 for (int k0 = 0; k0 < a.n_p; k0 += B) {
                     f32x4_t ok[B];
                     float mk[B], lk[B];
@@ -789,12 +845,13 @@ __device__ int fused_gen_item(const AttnArgs &a, int item, char *lds, int *s_lis
             fold_slot(Mg, Lg, Og, M, Ls, O);   // this item's slot, a.n_p, comes last
             write_row(a, cq * a.Hq + g * G + h, d, D, M, Ls, O);
         });
-        if ((int)threadIdx.x < n_pairs)
+        if ((int)threadIdx.x < n_pairs && cell_active(a, c0 + threadIdx.x))
             __hip_atomic_store(a.counters + (c0 + threadIdx.x) * a.Hkv + g, 0, __ATOMIC_RELAXED,
                                __HIP_MEMORY_SCOPE_AGENT);
         if (threadIdx.x == 0) s_list[0] = 0;   // nothing left to merge
     } else {
         waves_merge<D, G, NW>(S, lds, wpp, n_pairs, [&](int q, int h, int d, float M, float Lsum, f32x4_t O) {
+            if (!cell_active(a, c0 + q)) return;
             const uint32_t slot = slot_off(a, c0 + q, g, a.n_p);
             part_store4(r, slot + (uint32_t)(h * D + d) * 4u, O);
             if (d == 0) {
@@ -803,7 +860,7 @@ __device__ int fused_gen_item(const AttnArgs &a, int item, char *lds, int *s_lis
             }
         });
         stores_performed();
-        if ((int)threadIdx.x < n_pairs && arrive(a, c0 + threadIdx.x, g))
+        if ((int)threadIdx.x < n_pairs && cell_active(a, c0 + threadIdx.x) && arrive(a, c0 + threadIdx.x, g))
             s_list[1 + atomicAdd(&s_list[0], 1)] = c0 + threadIdx.x;
     }
     __syncthreads();

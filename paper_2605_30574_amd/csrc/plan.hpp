@@ -143,21 +143,21 @@ inline bool bf16_path(const splice_shape &sh) { return sh.dtype == SPLICE_BF16; 
 
 // bf16 row groups of one KV head: the rows of unspliced cells and the rows
 // of spliced cells are grouped separately (group_rows(D) rows per group), so
-// no group needs both the clean and the donor span.  n_clean cells of C are
-// unspliced at the call.
+// no group needs both the clean and the donor span.  n_clean of the call's
+// n_active cells (C, or the unfinished cells of a decode step) are unspliced.
 inline int clean_row_groups(const splice_shape &sh, int n_clean) {
     return ceil_div((int64_t)n_clean * group_of(sh), group_rows(sh.head_dim));
 }
-inline int row_groups(const splice_shape &sh, int n_clean) {
+inline int row_groups(const splice_shape &sh, int n_clean, int n_active) {
     return clean_row_groups(sh, n_clean) +
-           ceil_div((int64_t)(sh.n_cells - n_clean) * group_of(sh), group_rows(sh.head_dim));
+           ceil_div((int64_t)(n_active - n_clean) * group_of(sh), group_rows(sh.head_dim));
 }
 
 // Prompt work groups per prompt chunk.  The bf16 count depends on the call's
 // split of cells; the default chunking uses the split-independent bound
 // (one more row group than an unsplit grid).
 inline int prompt_items_per_chunk(const splice_shape &sh, int n_clean) {
-    return sh.n_kv_heads * (bf16_path(sh) ? row_groups(sh, n_clean) : sh.n_cells);
+    return sh.n_kv_heads * (bf16_path(sh) ? row_groups(sh, n_clean, sh.n_cells) : sh.n_cells);
 }
 inline int prompt_items_bound(const splice_shape &sh) {
     if (!bf16_path(sh)) return sh.n_kv_heads * sh.n_cells;
@@ -229,6 +229,16 @@ inline int gen_pairs(const splice_shape &sh, int n_gen) {
     return nw / wpp;
 }
 
+// Validation of a decode step's per-cell steps (host int32 [C]): each is
+// < gen_capacity; negative marks a finished cell.
+inline int32_t validate_steps(const splice_shape &sh, const int32_t *cell_step) {
+    if (sh.n_cells == 0) return SPLICE_OK;
+    if (!cell_step) return SPLICE_EINVAL;
+    for (int c = 0; c < sh.n_cells; ++c)
+        if (cell_step[c] >= sh.gen_capacity) return SPLICE_ESHAPE;
+    return SPLICE_OK;
+}
+
 // Cells of the call that are not spliced.
 inline int count_clean(const splice_shape &sh, const splice_call &call, const int32_t *cell_LW) {
     int n = 0;
@@ -236,9 +246,13 @@ inline int count_clean(const splice_shape &sh, const splice_call &call, const in
     return n;
 }
 
-inline AttnPlan plan_attn(const splice_shape &sh, const splice_call &call, int n_clean) {
+// Plan a call whose keys span `geo` (for a decode step with cells at
+// different steps: the widest visible prompt and the longest generated part)
+// over n_active cells, n_clean of them unspliced.
+inline AttnPlan plan_from_geo(const splice_shape &sh, const splice_call &call, const Geometry &geo, int n_clean,
+                              int n_active) {
     AttnPlan p;
-    p.geo = geometry(sh, call);
+    p.geo = geo;
     p.cellwise = !bf16_path(sh) && call.split_keys == 0 && p.geo.n_prompt <= kCellwiseMaxPrompt;
     if (p.cellwise) {
         p.n_p = p.n_g = 0;
@@ -260,7 +274,9 @@ inline AttnPlan plan_attn(const splice_shape &sh, const splice_call &call, int n
     p.n_slots = p.n_p + p.n_g;
     if (bf16_path(sh)) {
         // units (KV head, chunk) padded to whole rounds of kXcds, times row groups
-        p.n_prompt_items = kXcds * row_groups(sh, n_clean) * ceil_div((int64_t)sh.n_kv_heads * p.n_p, kXcds);
+        p.n_prompt_items = p.n_p > 0 ? kXcds * row_groups(sh, n_clean, n_active) *
+                                            ceil_div((int64_t)sh.n_kv_heads * p.n_p, kXcds)
+                                      : 0;
     } else {
         p.n_prompt_items = prompt_items_per_chunk(sh, n_clean) * p.n_p;
     }
@@ -284,6 +300,10 @@ inline bool gen_v_nontemporal(const splice_shape &sh) {
     const int64_t per_cache = (int64_t)sh.prompt_len * sh.n_kv_heads * sh.head_dim * elem_bytes(sh) * 2;
     const int64_t bytes = per_cache * (sh.donor_kind == SPLICE_DONOR_BUFFER ? 2 : 1);
     return bytes > kGenNtPromptBytes;
+}
+
+inline AttnPlan plan_attn(const splice_shape &sh, const splice_call &call, int n_clean) {
+    return plan_from_geo(sh, call, geometry(sh, call), n_clean, sh.n_cells);
 }
 
 struct WorkspaceLayout {

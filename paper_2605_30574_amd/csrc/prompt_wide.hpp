@@ -118,9 +118,13 @@ struct WideState {
 // One staged tile for this wave's RB row blocks.  A work group's rows all
 // belong to one class (unspliced or spliced cells), so every tile of its list
 // is visible to every row; rows past the last cell compute values that are
-// never stored.  Only a partial tile (n_valid < TK) masks keys.
+// never stored.  A partial tile (n_valid < TK) masks its missing keys; with
+// row_lo set, a row also masks the keys before its own first visible slot
+// lo[rb] (rows of cells at different steps under a sliding window), the
+// tile's first key being slot key0.
 template <int D, int RB>
-__device__ __forceinline__ void wide_compute(const char *buf, int n_valid,
+__device__ __forceinline__ void wide_compute(const char *buf, int n_valid, int key0, bool row_lo,
+                                             const int (&lo)[RB],
                                              const bf16x8_t (&qb)[RB][Wide<D, RB>::NDS], float qk_scale,
                                              WideState<D, RB> &S) {
     using X = Wide<D, RB>;
@@ -151,6 +155,13 @@ __device__ __forceinline__ void wide_compute(const char *buf, int n_valid,
             static_for<0, 2>([&](auto h) {
                 static_for<0, 4>([&](auto i) {
                     if (16 * h + 4 * quad + i >= n_valid) x[h][i] = -INFINITY;
+                });
+            });
+        }
+        if (row_lo) {   // uniform
+            static_for<0, 2>([&](auto h) {
+                static_for<0, 4>([&](auto i) {
+                    if (key0 + 16 * h + 4 * quad + i < lo[rb]) x[h][i] = -INFINITY;
                 });
             });
         }
@@ -189,7 +200,8 @@ __device__ __forceinline__ void wide_compute(const char *buf, int n_valid,
 
 template <int D, int RB, int DEPTH, int NT>
 __device__ __forceinline__ void wide_stream(const KeyList &L, const bf16x8_t (&qb)[RB][Wide<D, RB>::NDS],
-                                            float qk_scale, char *lds, WideState<D, RB> &S) {
+                                            float qk_scale, bool row_lo, const int (&lo)[RB], char *lds,
+                                            WideState<D, RB> &S) {
     using X = Wide<D, RB>;
     const int n_tiles = list_tiles(L);
     if (n_tiles == 0) return;
@@ -213,7 +225,7 @@ __device__ __forceinline__ void wide_stream(const KeyList &L, const bf16x8_t (&q
             ref[j] = list_tile_or_empty<X::TK>(L, t + DEPTH, n_tiles, X::ROW);
             wide_fetch<D, NT>(ref[j], r[j]);
             if (live) {
-                wide_compute<D, RB>(lds + (t & 1) * X::BUF, cur.n, qb, qk_scale, S);
+                wide_compute<D, RB>(lds + (t & 1) * X::BUF, cur.n, cur.key0, row_lo, lo, qb, qk_scale, S);
                 if (t + 1 < n_tiles) wide_stage<D, NT>(r[jn], lds + ((t + 1) & 1) * X::BUF);
                 __syncthreads();   // the next buffer is staged; nobody reads this one any more
             }

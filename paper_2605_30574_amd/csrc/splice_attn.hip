@@ -9,23 +9,25 @@
 // Kernels
 //   gather_kernel   splice_kv_build: bit-exact copy of each cell's visible
 //                   keys/values plus a source code per slot (16-byte moves).
-//   attn_kernel     splice_decode_attn, one launch per call, two kinds of
-//                   work item in one grid:
+//   fused_kernel    splice_decode_attn, bf16 inputs (attn_kernels.hpp): one
+//                   launch per call of two kinds of work item --
 //     prompt items  (KV head, 64 rows, prompt chunk): the rows are the
-//                   (cell, q head) pairs of all cells, clean cells first.
-//                   Each 64-key tile of the clean (and, for spliced rows,
-//                   the donor) prompt cache is staged in LDS once -- K
-//                   row-major, V transposed -- and feeds all 64 rows through
-//                   v_mfma_f32_16x16x32_bf16 for q.k and p.v.  (f32 inputs
-//                   take a per-cell vector-ALU variant.)
-//     generated items (cell, KV head, chunk of generated rows): lanes stream
-//                   the cell's own rows with coalesced 16-byte loads, D/16
-//                   lanes per row, v_dot2_f32_bf16 and a DPP butterfly for
-//                   q.k, per-row-group online softmax with lazy rescaling.
-//                   Generated rows are never spliced and are read once.
-//     Each item stores one partial (m, l, o) per row it serves; the last item
-//     of a (cell, KV head) to finish -- found with a device-scope counter --
-//     merges the partials and writes out and lse.
+//                   (cell, q head) pairs of all cells, clean cells first;
+//                   each 32-key tile of the clean (and, for spliced rows,
+//                   the donor) prompt cache is staged in LDS once for all 64
+//                   rows, and both products run on v_mfma_f32_16x16x32_bf16;
+//                   every row gets one partial (m, l, o) per chunk;
+//     generated-row items (KV head, a few cells): each cell's own rows
+//                   streamed on the matrix cores, never spliced, read once;
+//                   the item waits (bounded) for its cells' prompt partials
+//                   and merges them into out and lse.
+//                   splice_decode_step runs the same kernel with each cell
+//                   at its own step: the generated-row items first write the
+//                   current token's K/V row into the cell's cache, the prompt
+//                   items cover the widest visible prompt of the call and
+//                   mask, per row, what that row's step does not see, and
+//                   finished cells get no rows and no work.
+//   items_kernel, cellwise_kernel   f32 inputs, vector ALUs.
 //   fill_kernel     splice_workspace_init.
 //
 // ZERO donor: a ZERO slot has K = V = 0, so its score is exactly 0 and it
@@ -225,22 +227,37 @@ int32_t splice_workspace_init(void *workspace, size_t workspace_bytes, void *str
     return launch_status();
 }
 
-int32_t splice_decode_attn(const splice_shape *shape, const splice_call *call, const int32_t *cell_LW,
-                           const void *q, const void *clean_k, const void *clean_v,
-                           const void *donor_k, const void *donor_v, const void *gen_k,
-                           const void *gen_v, float *out, float *lse, void *workspace,
-                           size_t workspace_bytes, void *stream) {
+}  // extern "C"
+
+namespace {
+
+// splice_decode_attn (cell_step == nullptr: every cell at call->step) and
+// splice_decode_step (each cell at cell_step[c], k_new/v_new appended).
+int32_t decode_attn_impl(const splice_shape *shape, const splice_call *call, const int32_t *cell_LW,
+                         const int32_t *cell_step, const void *q, const void *k_new, const void *v_new,
+                         const void *clean_k, const void *clean_v, const void *donor_k, const void *donor_v,
+                         const void *gen_k, const void *gen_v, float *out, float *lse, void *workspace,
+                         size_t workspace_bytes, void *stream) {
     int32_t rc = splice::validate_shape(shape);
     if (rc != SPLICE_OK) return rc;
     const splice_shape &sh = *shape;
-    rc = splice::validate_call(sh, call);
+    if (!call) return SPLICE_EINVAL;
+    splice_call checked = *call;
+    if (cell_step) checked.step = 0;   // a decode step takes each cell's own step
+    rc = splice::validate_call(sh, &checked);
     if (rc != SPLICE_OK) return rc;
     rc = splice::validate_cells(sh, cell_LW);
     if (rc != SPLICE_OK) return rc;
+    const bool ragged = cell_step != nullptr;
+    if (ragged) {
+        rc = splice::validate_steps(sh, cell_step);
+        if (rc != SPLICE_OK) return rc;
+    }
     if (sh.n_cells == 0) return SPLICE_OK;
     const bool zero = sh.donor_kind == SPLICE_DONOR_ZERO;
     const bool has_prompt = sh.prompt_len > 0;   // an empty prompt has no prompt buffers to read
     if (!q || !gen_k || !gen_v || !out || !lse) return SPLICE_EINVAL;
+    if (ragged && (!k_new || !v_new)) return SPLICE_EINVAL;
     if (has_prompt && (!clean_k || !clean_v)) return SPLICE_EINVAL;
     if (zero ? (donor_k || donor_v) : (has_prompt && (!donor_k || !donor_v))) return SPLICE_EINVAL;
     const void *ptrs[] = {q, clean_k, clean_v, gen_k, gen_v};
@@ -248,9 +265,43 @@ int32_t splice_decode_attn(const splice_shape *shape, const splice_call *call, c
         if (!splice::aligned(p, 16)) return SPLICE_EINVAL;
     if (!zero && (!splice::aligned(donor_k, 16) || !splice::aligned(donor_v, 16))) return SPLICE_EINVAL;
     if (!splice::aligned(out, 16) || !splice::aligned(lse, 4)) return SPLICE_EINVAL;
+    if (ragged && (!splice::aligned(k_new, 16) || !splice::aligned(v_new, 16))) return SPLICE_EINVAL;
+    if (ragged && !splice::bf16_path(sh)) return SPLICE_EUNSUPPORTED;
 
-    const int n_clean = splice::count_clean(sh, *call, cell_LW);
-    const splice::AttnPlan plan = splice::plan_attn(sh, *call, n_clean);
+    // the steps of the call: one for every cell, or each cell's own
+    auto step_of = [&](int c) { return ragged ? cell_step[c] : call->step; };
+    int s_min = INT32_MAX, s_max = -1, n_active = 0;
+    for (int c = 0; c < sh.n_cells; ++c) {
+        const int s = step_of(c);
+        if (s < 0) continue;
+        ++n_active;
+        s_min = s < s_min ? s : s_min;
+        s_max = s > s_max ? s : s_max;
+    }
+    if (n_active == 0) return SPLICE_OK;   // every cell finished
+    splice_call lo_call = *call, hi_call = *call;
+    lo_call.step = s_min;
+    hi_call.step = s_max;
+    const splice::Geometry g_lo = splice::geometry(sh, lo_call), g_hi = splice::geometry(sh, hi_call);
+    // widest visible prompt (the smallest step) and longest generated part (the largest)
+    splice::Geometry geo = g_hi;
+    geo.jp0 = g_lo.jp0;
+    geo.sa = g_lo.sa;
+    geo.sb = g_lo.sb;
+    geo.n_prompt = g_lo.n_prompt;
+    geo.n_vis = geo.n_prompt + geo.n_gen;
+
+    int n_clean = 0;
+    uint32_t spliced[SPLICE_MAX_CELLS / 32] = {0};
+    for (int c = 0; c < sh.n_cells; ++c) {
+        const int s = step_of(c);
+        if (s < 0) continue;
+        if (splice::cell_spliced(cell_LW, c, call->layer, s))
+            spliced[c >> 5] |= 1u << (c & 31);
+        else
+            ++n_clean;
+    }
+    const splice::AttnPlan plan = splice::plan_from_geo(sh, hi_call, geo, n_clean, n_active);
     if (plan.n_slots > splice::kMaxSlots) return SPLICE_EUNSUPPORTED;
     const splice::WorkspaceLayout wl = splice::workspace_layout(sh, plan.n_slots);
     if (!workspace || !splice::aligned(workspace, 256)) return SPLICE_EWORKSPACE;
@@ -260,12 +311,12 @@ int32_t splice_decode_attn(const splice_shape *shape, const splice_call *call, c
     const AttnKernels kern = pick_attn(sh.head_dim, G, sh.dtype);
     if (!kern.items) return SPLICE_EUNSUPPORTED;
 
-    const splice::Geometry &geo = plan.geo;
     AttnArgs a;
     a.q = (const char *)q;
     a.ck = (const char *)clean_k; a.cv = (const char *)clean_v;
     a.dk = (const char *)donor_k; a.dv = (const char *)donor_v;
     a.gk = (const char *)gen_k; a.gv = (const char *)gen_v;
+    a.kn = (const char *)k_new; a.vn = (const char *)v_new;
     a.out = out; a.lse = lse;
     a.counters = (int *)((char *)workspace + wl.counters_off);
     a.part = (float *)((char *)workspace + wl.part_off);
@@ -278,22 +329,31 @@ int32_t splice_decode_attn(const splice_shape *shape, const splice_call *call, c
     a.n_p = plan.n_p; a.p_len = plan.p_len; a.n_g = plan.n_g; a.g_len = plan.g_len;
     a.n_slots = plan.n_slots;
     a.slot_floats = splice::slot_floats(G, sh.head_dim);
-    a.n_rb = splice::bf16_path(sh) ? splice::row_groups(sh, n_clean) : 0;
-    a.n_rg_clean = splice::bf16_path(sh) ? splice::clean_row_groups(sh, n_clean) : 0;
+    a.n_rb = 0; a.n_rg_clean = 0;
     a.n_prompt_items = plan.n_prompt_items;
     a.gen_pairs = plan.gen_pairs;
     a.gen_v_nt = splice::gen_v_nontemporal(sh) ? 1 : 0;
     a.wait_polls = call->merge_wait == 0 ? kDefaultWaitPolls : (call->merge_wait < 0 ? 0 : call->merge_wait);
     a.qk_scale = call->scale * kLog2e;
-    fill_mask(sh, *call, cell_LW, a.spliced);
-    // row-block order: clean cells first, then spliced cells (each by index)
+    a.ragged = ragged ? 1 : 0;
+    a.window = call->window;
+    a.span_lo = sh.span_lo; a.span_hi = sh.span_hi;
+    a.row_lo = ragged && g_lo.jp0 != g_hi.jp0 ? 1 : 0;
+    for (int i = 0; i < SPLICE_MAX_CELLS / 32; ++i) a.spliced[i] = spliced[i];
+    for (int c = 0; c < SPLICE_MAX_CELLS; ++c) a.cstep[c] = c < sh.n_cells ? step_of(c) : -1;
+    // row-block order: active clean cells first, then active spliced cells (each by index)
     int n = 0;
     for (int c = 0; c < sh.n_cells; ++c)
-        if (!splice::cell_spliced(cell_LW, c, call->layer, call->step)) a.order[n++] = (uint8_t)c;
+        if (step_of(c) >= 0 && !(spliced[c >> 5] >> (c & 31) & 1u)) a.order[n++] = (uint8_t)c;
     a.n_clean = n;
     for (int c = 0; c < sh.n_cells; ++c)
-        if (splice::cell_spliced(cell_LW, c, call->layer, call->step)) a.order[n++] = (uint8_t)c;
+        if (step_of(c) >= 0 && (spliced[c >> 5] >> (c & 31) & 1u)) a.order[n++] = (uint8_t)c;
+    a.n_active = n;
     for (; n < SPLICE_MAX_CELLS; ++n) a.order[n] = 0;
+    if (splice::bf16_path(sh)) {
+        a.n_rb = splice::row_groups(sh, a.n_clean, a.n_active);
+        a.n_rg_clean = splice::clean_row_groups(sh, a.n_clean);
+    }
 
     if (plan.cellwise) {
         hipLaunchKernelGGL(kern.cellwise, dim3((unsigned)(sh.n_cells * sh.n_kv_heads)), dim3(kThreads), 0,
@@ -305,6 +365,29 @@ int32_t splice_decode_attn(const splice_shape *shape, const splice_call *call, c
     const int threads = splice::bf16_path(sh) ? 64 * splice::fused_waves(sh.head_dim) : kThreads;
     hipLaunchKernelGGL(kern.items, dim3((unsigned)items), dim3((unsigned)threads), 0, (hipStream_t)stream, a);
     return launch_status();
+}
+
+}  // namespace
+
+extern "C" {
+
+int32_t splice_decode_attn(const splice_shape *shape, const splice_call *call, const int32_t *cell_LW,
+                           const void *q, const void *clean_k, const void *clean_v,
+                           const void *donor_k, const void *donor_v, const void *gen_k,
+                           const void *gen_v, float *out, float *lse, void *workspace,
+                           size_t workspace_bytes, void *stream) {
+    return decode_attn_impl(shape, call, cell_LW, nullptr, q, nullptr, nullptr, clean_k, clean_v, donor_k,
+                            donor_v, gen_k, gen_v, out, lse, workspace, workspace_bytes, stream);
+}
+
+int32_t splice_decode_step(const splice_shape *shape, const splice_call *call, const int32_t *cell_LW,
+                           const int32_t *cell_step, const void *q, const void *k_new, const void *v_new,
+                           const void *clean_k, const void *clean_v, const void *donor_k,
+                           const void *donor_v, void *gen_k, void *gen_v, float *out, float *lse,
+                           void *workspace, size_t workspace_bytes, void *stream) {
+    if (!cell_step && shape && shape->n_cells > 0) return SPLICE_EINVAL;
+    return decode_attn_impl(shape, call, cell_LW, cell_step, q, k_new, v_new, clean_k, clean_v, donor_k,
+                            donor_v, gen_k, gen_v, out, lse, workspace, workspace_bytes, stream);
 }
 
 }  // extern "C"

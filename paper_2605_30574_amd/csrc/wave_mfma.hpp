@@ -41,6 +41,7 @@ struct KeyList {
     const char *v[kMaxSeg];
     int len[kMaxSeg];
     int cols[kMaxSeg];             // SegCols
+    int key0[kMaxSeg];             // position of the segment's first key (prompt slots)
     int first_tile[kMaxSeg + 1];   // tiles before segment s; [n_seg] = total
     int n_seg;
 };
@@ -55,6 +56,7 @@ __device__ __forceinline__ void list_init(KeyList &L) {
         L.v[s] = nullptr;
         L.len[s] = 0;
         L.cols[s] = kColsAll;
+        L.key0[s] = 0;
     }
 }
 
@@ -63,7 +65,8 @@ __device__ __forceinline__ void list_init(KeyList &L) {
 // takes constant values after unrolling, so the list stays in scalar
 // registers.
 template <int TK = kTileKeys>
-__device__ __forceinline__ void list_add(KeyList &L, const char *k, const char *v, int n, int cols = kColsAll) {
+__device__ __forceinline__ void list_add(KeyList &L, const char *k, const char *v, int n, int cols = kColsAll,
+                                         int key0 = 0) {
     if (n <= 0) return;
     const int tiles = (n + TK - 1) / TK;
 #pragma unroll
@@ -73,6 +76,7 @@ __device__ __forceinline__ void list_add(KeyList &L, const char *k, const char *
             L.v[s] = v;
             L.len[s] = n;
             L.cols[s] = cols;
+            L.key0[s] = key0;
             L.first_tile[s + 1] = L.first_tile[s] + tiles;
         } else if (s > L.n_seg) {
             L.first_tile[s + 1] = L.first_tile[s] + tiles;
@@ -89,17 +93,18 @@ __device__ __forceinline__ int list_tiles(const KeyList &L) {
     return t;
 }
 
-// Where tile t lies: base pointers of its first key, its valid key count and
-// which columns see it.
+// Where tile t lies: base pointers of its first key, its valid key count,
+// which columns see it and the position of its first key.
 struct TileRef {
     const char *k, *v;
     int n;
     int cols;
+    int key0;
 };
 
 template <int TK = kTileKeys>
 __device__ __forceinline__ TileRef list_tile(const KeyList &L, int t, int row_bytes) {
-    TileRef r{L.k[0], L.v[0], 0, kColsAll};
+    TileRef r{L.k[0], L.v[0], 0, kColsAll, 0};
     int off = t;
 #pragma unroll
     for (int s = 0; s < kMaxSeg; ++s) {
@@ -109,12 +114,14 @@ __device__ __forceinline__ TileRef list_tile(const KeyList &L, int t, int row_by
             r.v = L.v[s];
             r.n = L.len[s];
             r.cols = L.cols[s];
+            r.key0 = L.key0[s];
         }
     }
     const int t0 = off * TK;
     r.k += (size_t)t0 * row_bytes;
     r.v += (size_t)t0 * row_bytes;
     r.n = min(TK, r.n - t0);
+    r.key0 += t0;
     return r;
 }
 
@@ -122,7 +129,7 @@ __device__ __forceinline__ TileRef list_tile(const KeyList &L, int t, int row_by
 // row load returns 0 without a memory access.  Issuing loads for it keeps the
 // number of loads in flight the same on every path, which lets the compiler
 // wait for exactly the tile it needs instead of for all of them.
-__device__ __forceinline__ TileRef empty_tile(const KeyList &L) { return TileRef{L.k[0], L.v[0], 0, kColsAll}; }
+__device__ __forceinline__ TileRef empty_tile(const KeyList &L) { return TileRef{L.k[0], L.v[0], 0, kColsAll, 0}; }
 
 template <int TK = kTileKeys>
 __device__ __forceinline__ TileRef list_tile_or_empty(const KeyList &L, int t, int n_tiles, int row_bytes) {

@@ -24,10 +24,11 @@ SPLICE_DONOR_BUFFER, SPLICE_DONOR_ZERO = 0, 1
 SPLICE_BF16, SPLICE_F32 = 0, 1
 SPLICE_SRC_CLEAN, SPLICE_SRC_DONOR, SPLICE_SRC_ZERO, SPLICE_SRC_GEN = 0, 1, 2, 3
 SPLICE_MAX_CELLS = 256
-SPLICE_ABI_VERSION = 2   # layout of SpliceShape / SpliceCall below
+SPLICE_ABI_VERSION = 3   # layout of SpliceShape / SpliceCall below
 
 EXPORTS = ("splice_abi_version", "splice_status_str", "splice_visible_len", "splice_kv_build",
-           "splice_decode_attn_workspace_bytes", "splice_workspace_init", "splice_decode_attn")
+           "splice_decode_attn_workspace_bytes", "splice_workspace_init", "splice_decode_attn",
+           "splice_decode_step")
 
 
 class SpliceShape(ctypes.Structure):
@@ -77,6 +78,9 @@ def load_library(path: str = LIB_PATH):
     lib.splice_decode_attn.restype = i32
     lib.splice_decode_attn.argtypes = [shp, cal, i32p, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp,
                                        ctypes.c_size_t, vp]
+    lib.splice_decode_step.restype = i32
+    lib.splice_decode_step.argtypes = [shp, cal, i32p, i32p, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp,
+                                       vp, ctypes.c_size_t, vp]
     got = lib.splice_abi_version()
     if got != SPLICE_ABI_VERSION:
         raise ImportError(f"{path} has ABI version {got}, this binding expects {SPLICE_ABI_VERSION}: rebuild it")
@@ -243,3 +247,40 @@ def splice_decode_attn(shape: SpliceShape, call: SpliceCall, cell_LW, q, clean_k
     lw, lwp = _cells(cell_LW, C)
     _check(lib.splice_decode_attn(ctypes.byref(shape), ctypes.byref(call), lwp, qp, ck, cv, dk, dv, gk, gv,
                                   op, lp, wp, wbytes, _stream_ptr(stream, dev)), "splice_decode_attn")
+
+
+def _steps(cell_step, n_cells: int):
+    a = np.ascontiguousarray(np.asarray(cell_step, dtype=np.int32).reshape(-1))
+    if a.shape[0] != n_cells:
+        raise ValueError(f"cell_step has {a.shape[0]} entries, shape says {n_cells} cells")
+    return a, a.ctypes.data_as(ctypes.POINTER(ctypes.c_int32))
+
+
+def splice_decode_step(shape: SpliceShape, call: SpliceCall, cell_LW, cell_step, q, k_new, v_new, clean_k,
+                       clean_v, donor_k, donor_v, gen_k, gen_v, out, lse, workspace, stream=None) -> None:
+    """One decode pass with each cell at its own step ``cell_step[c]`` (< 0: finished).
+
+    Appends ``k_new[c]``, ``v_new[c]`` ([C, Hkv, D]) as row ``cell_step[c]`` of the
+    cell's generated caches, then attends as ``splice_decode_attn`` at that step.
+    """
+    import torch
+    lib = load_library()
+    C, Hq, Hkv, D = shape.n_cells, shape.n_q_heads, shape.n_kv_heads, shape.head_dim
+    dt = _torch_dtype(shape)
+    n_prompt = Hkv * shape.prompt_len * D
+    qp, dev = _dev_ptr(q, "q", C * Hq * D, dt)
+    kn, _ = _dev_ptr(k_new, "k_new", C * Hkv * D, dt, dev)
+    vn, _ = _dev_ptr(v_new, "v_new", C * Hkv * D, dt, dev)
+    ck, _ = _dev_ptr(clean_k, "clean_k", n_prompt, dt, dev)
+    cv, _ = _dev_ptr(clean_v, "clean_v", n_prompt, dt, dev)
+    dk, dv = _donors(shape, donor_k, donor_v, dt, n_prompt, dev)
+    gk, _ = _dev_ptr(gen_k, "gen_k", C * Hkv * shape.gen_capacity * D, dt, dev)
+    gv, _ = _dev_ptr(gen_v, "gen_v", C * Hkv * shape.gen_capacity * D, dt, dev)
+    op, _ = _dev_ptr(out, "out", C * Hq * D, torch.float32, dev)
+    lp, _ = _dev_ptr(lse, "lse", C * Hq, torch.float32, dev)
+    wp, _ = _dev_ptr(workspace, "workspace", None, None, dev)
+    wbytes = workspace.numel() * workspace.element_size()
+    lw, lwp = _cells(cell_LW, C)
+    st, stp = _steps(cell_step, C)
+    _check(lib.splice_decode_step(ctypes.byref(shape), ctypes.byref(call), lwp, stp, qp, kn, vn, ck, cv, dk, dv,
+                                  gk, gv, op, lp, wp, wbytes, _stream_ptr(stream, dev)), "splice_decode_step")

@@ -25,7 +25,7 @@ def test_library_exports_every_declared_symbol():
     lib = sp.load_library()
     for name in declared:
         assert hasattr(lib, name), name
-    assert sp.splice_abi_version() == 2
+    assert sp.splice_abi_version() == 3
 
 
 def test_single_hip_runtime_mapped():
@@ -149,3 +149,32 @@ def test_workspace_bound_covers_every_call():
             for window in (0, 1, 1024):
                 need = sp.splice_decode_attn_workspace_bytes(sh, sp.make_call(0, step, window, 1.0))
                 assert need <= worst, (C, Hkv, Tp, cap, step, window)
+
+
+def test_decode_step_validation_before_device_access():
+    lib = sp.load_library()
+    sh = _shape(dtype="bf16")
+    call = sp.make_call(1, 999, 0, 0.125)   # step is ignored by a decode step
+    lw = (ctypes.c_int32 * 12)(*([0, 0] * 6))
+    fake = ctypes.c_void_p(0x1000)   # never dereferenced: validation fails first
+    ws = ctypes.c_void_p(0x2000)
+    need = sp.splice_decode_attn_workspace_bytes(sh)
+
+    def step(shape, steps, kn=fake, vn=fake, wbytes=need):
+        st = None if steps is None else (ctypes.c_int32 * len(steps))(*steps)
+        return lib.splice_decode_step(ctypes.byref(shape), ctypes.byref(call), lw, st, fake, kn, vn, fake, fake,
+                                      None, None, fake, fake, fake, fake, ws, wbytes, None)
+
+    assert step(sh, None) == sp.SPLICE_EINVAL                          # cell_step required
+    assert step(sh, [0, 1, 2, 3, 4, 16]) == sp.SPLICE_ESHAPE           # s_c >= gen_capacity
+    assert step(sh, [0, 1, 2, 3, 4, 5], kn=None) == sp.SPLICE_EINVAL   # new rows required
+    assert step(sh, [0, 1, 2, 3, 4, 5], vn=ctypes.c_void_p(0x1004)) == sp.SPLICE_EINVAL   # misaligned
+    assert step(sh, [0, 1, 2, 3, 4, 5], wbytes=16) == sp.SPLICE_EWORKSPACE
+    assert step(_shape(dtype="f32"), [0, 1, 2, 3, 4, 5]) == sp.SPLICE_EUNSUPPORTED
+    # every cell finished: a valid call with nothing to do (nothing launched)
+    assert step(sh, [-1] * 6) == sp.SPLICE_OK
+    # the call's own step is not validated, its other fields are
+    bad = sp.make_call(2, 0, 0, 0.125)
+    st = (ctypes.c_int32 * 6)(*([0] * 6))
+    assert lib.splice_decode_step(ctypes.byref(sh), ctypes.byref(bad), lw, st, fake, fake, fake, fake, fake, None,
+                                  None, fake, fake, fake, fake, ws, need, None) == sp.SPLICE_ESHAPE

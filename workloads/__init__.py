@@ -5,7 +5,9 @@ and the random-input recipe, and none of the method's arithmetic.
 """
 from .configs import (DONOR_BLANK, DONOR_DIFF, DONOR_ZERO, WORKLOADS, Workload,
                       get)
-from .inputs import cell_lw, derive_seed, make_layer, make_q, to_numpy, torch_dtype
+from .inputs import (cell_lw, cell_steps, derive_seed, make_layer, make_new_rows, make_q, to_numpy,
+                     torch_dtype)
 
 __all__ = ["DONOR_BLANK", "DONOR_DIFF", "DONOR_ZERO", "WORKLOADS", "Workload", "get",
-           "cell_lw", "derive_seed", "make_layer", "make_q", "to_numpy", "torch_dtype"]
+           "cell_lw", "cell_steps", "derive_seed", "make_layer", "make_new_rows", "make_q", "to_numpy",
+           "torch_dtype"]

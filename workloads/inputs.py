@@ -29,6 +29,7 @@ from .configs import DONOR_BLANK, DONOR_DIFF, DONOR_ZERO, Workload
 
 # tensor kinds, one seed stream each
 KIND_Q, KIND_CLEAN_K, KIND_CLEAN_V, KIND_DONOR_K, KIND_DONOR_V, KIND_GEN_K, KIND_GEN_V = range(7)
+KIND_NEW_K, KIND_NEW_V, KIND_STEPS = 7, 8, 9
 
 
 def derive_seed(base: int, workload_index: int, kind: int, layer: int, step: int = 0) -> int:
@@ -95,6 +96,34 @@ def make_q(w: Workload, layer: int, step: int, seed: int = 0, device="cpu",
     C = w.n_cells if n_cells is None else n_cells
     q = _randn((C, w.n_q_heads, w.head_dim), derive_seed(seed, w.index, KIND_Q, layer, step), device)
     return q.to(torch_dtype(w)).contiguous()
+
+
+def make_new_rows(w: Workload, layer: int, step: int, seed: int = 0, device="cpu",
+                  n_cells: Optional[int] = None) -> Dict[str, torch.Tensor]:
+    """The K, V rows [C][Hkv][D] the current token of every cell appends at one
+    decode pass (drawn like generated rows)."""
+    C = w.n_cells if n_cells is None else n_cells
+    shp = (C, w.n_kv_heads, w.head_dim)
+    kn = _finish_k(w, _randn(shp, derive_seed(seed, w.index, KIND_NEW_K, layer, step), device), False)
+    vn = _randn(shp, derive_seed(seed, w.index, KIND_NEW_V, layer, step), device)
+    dt = torch_dtype(w)
+    return dict(k_new=kn.to(dt).contiguous(), v_new=vn.to(dt).contiguous())
+
+
+def cell_steps(w: Workload, seed: int = 0, n_cells: Optional[int] = None, finished: float = 0.125,
+               max_step: Optional[int] = None) -> np.ndarray:
+    """int32 [C]: a mix of per-cell decode steps, as in a batch whose slots are
+    refilled with new cells as others stop -- uniform in [0, max_step], about
+    ``finished`` of the cells stopped (-1), and steps 0 and max_step present
+    when there are at least two cells."""
+    C = w.n_cells if n_cells is None else n_cells
+    top = w.n_steps - 1 if max_step is None else max_step
+    rng = np.random.default_rng(derive_seed(seed, w.index, KIND_STEPS, 0))
+    st = rng.integers(0, top + 1, size=C).astype(np.int32)
+    st[rng.random(C) < finished] = -1
+    if C >= 2:
+        st[0], st[C - 1] = 0, top
+    return np.ascontiguousarray(st)
 
 
 def cell_lw(w: Workload, cells=None) -> np.ndarray:
