@@ -23,7 +23,12 @@ Reported (one JSON line):
               counter summary when it was taken on the current kernel source
               (else null);
   cpu_baseline  the fp64 oracle timed on this host's cores on a stratified
-              sample of the same workload's calls.
+              sample of the same workload's calls;
+  decode_step  splice_decode_step passes (each cell at its own step, the
+              current token's K/V appended, finished cells skipped) over two
+              seeded step mixes -- 1/8 and 1/2 of the cells finished --
+              measured after the timed region: time per launch, GB/s of
+              the pass's algorithmic bytes, active cells, cell-steps/s.
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--config qwen3-4b]
 """
@@ -86,6 +91,41 @@ def call_bytes(w, layer: int, step: int, spliced_flags) -> int:
     total += (n_sv * row) if (any_spl and buffer_donor) else 0  # donor span
     total += C * n_gen * row                                    # generated rows
     total += C * w.n_q_heads * (4 * w.head_dim + 4)             # out + lse
+    return total
+
+
+def step_bytes(w, layer: int, steps, cells) -> int:
+    """Bytes a splice_decode_step call must move at minimum: the prompt slots
+    some active cell sees (each once), each active cell's visible generated
+    rows before its own step, its new K/V row read and written once, q, out
+    and lse of the active cells.  Finished cells (step < 0) move nothing."""
+    e = w.elem_bytes
+    row = 2 * w.n_kv_heads * w.head_dim * e
+    Tp, (a, b) = w.prompt_len, w.span
+    win = w.window(layer)
+    act = [(s, L, W) for s, (L, W) in zip(steps, cells) if s >= 0]
+    if not act:
+        return 0
+    total = 0
+    vis = [0] * Tp                       # per prompt slot: 1 clean read, 2 donor read (bit mask)
+    for s, L, W in act:
+        p = Tp + s
+        j0 = p - win + 1 if win > 0 else 0
+        jp0 = min(max(j0, 0), Tp)
+        i0 = max(0, j0 - Tp)
+        total += (s - i0) * row + 2 * row                        # cached rows, new row in and out
+        spl = layer >= L and s >= W
+        donor_read = spl and w.donor != "zero"
+        for j in range(jp0, Tp):
+            in_span = a <= j < b
+            if not in_span or not spl:
+                vis[j] |= 1
+            elif donor_read:
+                vis[j] |= 2
+    total += sum(bin(v).count("1") for v in vis) * row           # prompt slots, once per source
+    n_act = len(act)
+    total += n_act * w.n_q_heads * w.head_dim * e                  # q
+    total += n_act * w.n_q_heads * (4 * w.head_dim + 4)            # out + lse
     return total
 
 
@@ -292,6 +332,49 @@ def main():
     log("per-step buckets: " + ", ".join(f"s={k}: {v['us_per_launch']} us/launch, {v['GB/s']} GB/s"
                                           for k, v in per_step.items()))
 
+    # decode passes with cells at their own steps (splice_decode_step: KV
+    # append + attention, finished cells skipped), outside the timed region:
+    # one pass = the N layers' launches, graph-captured like the sweep steps
+    decode_step = None
+    if w.dtype == "bf16":
+        mixes = {"ragged": workloads.cell_steps(w, seed=1, n_cells=C, finished=0.125),
+                 "ragged-half-finished": workloads.cell_steps(w, seed=2, n_cells=C, finished=0.5)}
+        news = [workloads.make_new_rows(w, l, 0, device=dev) for l in range(N)]
+        call0 = [sp.make_call(l, 0, w.window(l), w.scale) for l in range(N)]
+        decode_step = {}
+        for name, st in mixes.items():
+            def issue_pass(st=st):
+                for l in range(N):
+                    b = layers[l]
+                    sp.splice_decode_step(shape, call0[l], lw, st, qs[l], news[l]["k_new"], news[l]["v_new"],
+                                          b["clean_k"], b["clean_v"], b["donor_k"], b["donor_v"],
+                                          b["gen_k"], b["gen_v"], out, lse, ws)
+            g = None
+            if not args.eager:
+                g = torch.cuda.CUDAGraph()
+                with torch.cuda.graph(g, stream=stream):
+                    issue_pass()
+            reps = 10
+            with torch.cuda.stream(stream):
+                (g.replay() if g else issue_pass())
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            torch.cuda.synchronize()
+            e0.record(stream)
+            with torch.cuda.stream(stream):
+                for _ in range(reps):
+                    (g.replay() if g else issue_pass())
+            e1.record(stream)
+            torch.cuda.synchronize()
+            t = e0.elapsed_time(e1) / 1e3 / reps
+            bts = sum(step_bytes(w, l, st.tolist(), w.cells) for l in range(N))
+            act = st[st >= 0]
+            decode_step[name] = {"us_per_launch": round(t / N * 1e6, 2), "GB/s": round(bts / t / 1e9, 1),
+                                 "active_cells": int(act.size), "mean_step": round(float(act.mean()), 1),
+                                 "cell_steps_per_s": round(int(act.size) / t, 1)}
+        log("decode passes: " + ", ".join(f"{k}: {v['us_per_launch']} us/launch, {v['GB/s']} GB/s, "
+                                           f"{v['active_cells']} active" for k, v in decode_step.items()))
+
     traffic, traffic_src = stored_traffic(w.name)
     per_launch_bytes = alg_bytes / launches
     avg_launch_s = sec / launches
@@ -324,6 +407,7 @@ def main():
         "roofline": roofline,
         "cpu_baseline": cpu,
         "per_step": per_step,
+        "decode_step": decode_step,
     }
     print(json.dumps(res), flush=True)
 
