@@ -150,28 +150,38 @@ def cpu_baseline(w, seconds_cap: float = 30.0):
     import workloads
     N, S = w.n_layers, w.n_steps
     layers = sorted({0, N // 2, N - 1})
-    n_s = min(S, 64)
-    steps = sorted({min(S - 1, int((i + 0.5) * S / n_s)) for i in range(n_s)})
     lw = workloads.cell_lw(w)
     osh = oracle.shape_of(w)
     lib = oracle.load()
     threads = oracle.max_threads()
+
+    def one_call(hb, layer, step):
+        q = workloads.to_numpy(workloads.make_q(w, layer, step, device="cpu"))
+        t0 = time.perf_counter()
+        oracle.attn(osh, layer, step, w.window(layer), w.scale, lw, q, hb["clean_k"], hb["clean_v"],
+                    hb["donor_k"], hb["donor_v"], hb["gen_k"], hb["gen_v"], n_threads=threads, lib=lib)
+        return time.perf_counter() - t0
+
+    # pilot (untimed): one call at the middle step sizes the stratified grid
+    # so that the sample takes about seconds_cap; a call's cost is affine in
+    # the step, so the middle step is the grid's average
+    hb = {k: workloads.to_numpy(v) for k, v in workloads.make_layer(w, layers[0], device="cpu").items()}
+    t_mid = max(one_call(hb, layers[0], S // 2), 1e-4)
+    n_s = int(max(4, min(S, seconds_cap / (len(layers) * t_mid))))
+    steps = sorted({min(S - 1, int((i + 0.5) * S / n_s)) for i in range(n_s)})
     done_bytes, done_time, n_calls = 0, 0.0, 0
     t_start = time.time()
     for layer in layers:
-        hb = {k: workloads.to_numpy(v) for k, v in workloads.make_layer(w, layer, device="cpu").items()}
+        if layer != layers[0]:
+            hb = {k: workloads.to_numpy(v) for k, v in workloads.make_layer(w, layer, device="cpu").items()}
         for step in steps:
-            q = workloads.to_numpy(workloads.make_q(w, layer, step, device="cpu"))
-            t0 = time.perf_counter()
-            oracle.attn(osh, layer, step, w.window(layer), w.scale, lw, q, hb["clean_k"], hb["clean_v"],
-                        hb["donor_k"], hb["donor_v"], hb["gen_k"], hb["gen_v"], n_threads=threads, lib=lib)
-            done_time += time.perf_counter() - t0
+            done_time += one_call(hb, layer, step)
             done_bytes += call_bytes(w, layer, step, spliced_flags(w, layer, step))
             n_calls += 1
-            if time.time() - t_start > seconds_cap:
+            if time.time() - t_start > 2 * seconds_cap:   # a bad pilot estimate: stop the sample
                 break
         del hb
-        if time.time() - t_start > seconds_cap:
+        if time.time() - t_start > 2 * seconds_cap:
             break
     gbs = done_bytes / done_time / 1e9
     return {"value": round(gbs, 4), "unit": "GB/s", "cores": threads, "kind": "oracle",
