@@ -573,8 +573,8 @@ __global__ __launch_bounds__(kThreads) void items_kernel(AttnArgs a) {
 constexpr int kDefaultWaitPolls = 16384;
 
 // Work-group shape: NW waves (splice::fused_waves), NT threads, ROWS rows
-// of a prompt item.  Tiles in flight: the prompt items' register ring and
-// each generated-row wave, within the registers a lane has at
+// of a prompt item.  Tiles in flight: the prompt items' LDS ring, and the
+// registers of each generated-row wave, within the registers a lane has at
 // WAVES_PER_SIMD waves per SIMD (168 at 3, 256 at 2).
 template <int D>
 struct Fused {
@@ -582,7 +582,6 @@ struct Fused {
     static constexpr int NT = NW * 64;
     static constexpr int RB = splice::fused_row_blocks(D);
     static constexpr int ROWS = splice::group_rows(D);
-    static constexpr int PROMPT_DEPTH = D <= 128 ? 3 : 2;
     static constexpr int GEN_DEPTH = D <= 128 ? 2 : 1;
     static constexpr int WAVES_PER_SIMD = D <= 128 ? 3 : 2;
     static_assert(ROWS == NW * 16 * RB, "host and device agree on the row groups");
@@ -620,7 +619,7 @@ __device__ __forceinline__ void merge_slots_once(const AttnArgs &a, __amdgpu_buf
 template <int D, int G>
 struct FusedLds {
     static constexpr int NW = Fused<D>::NW;
-    static constexpr int PROMPT = Wide<D, Fused<D>::RB>::LDS;
+    static constexpr int PROMPT = Direct<D>::LDS;
     static constexpr int WAVE_MERGE = NW * G * (D + 2) * 4;                     // waves_merge buffer
     static constexpr int GEN = cmax(NW * WaveMfma<D>::LDS, WAVE_MERGE);         // V^T tiles, wave merge
     static constexpr int MERGE = 2 * kRowBlock * kMaxSlots * 4;                 // combine_cells staging
@@ -644,7 +643,7 @@ template <int D, int G>
 __device__ int fused_prompt_item(const AttnArgs &a, int item, char *lds, int *s_list) {
     constexpr int RB = Fused<D>::RB, ROWS = Fused<D>::ROWS;
     constexpr int X8 = splice::kXcds;
-    using X = Wide<D, RB>;
+    using X = Direct<D>;
     const int rg = (item / X8) % a.n_rb;
     const int u = (item / X8 / a.n_rb) * X8 + item % X8;
     if (u >= a.n_p * a.Hkv) return 0;   // s_list[0] stays 0: nothing to merge
@@ -695,7 +694,7 @@ __device__ int fused_prompt_item(const AttnArgs &a, int item, char *lds, int *s_
         S.m[rb] = -INFINITY;
         S.lsum[rb] = 0.f;
     });
-    wide_stream<D, RB, Fused<D>::PROMPT_DEPTH, Fused<D>::NT>(L, qb, a.qk_scale, a.row_lo != 0, lo, lds, S);
+    direct_stream<D, RB, Fused<D>::NW>(L, qb, a.qk_scale, a.row_lo != 0, lo, lds, S);
 
     const __amdgpu_buffer_rsrc_t r = part_rsrc(a);
     static_for<0, RB>([&](auto rb) {
