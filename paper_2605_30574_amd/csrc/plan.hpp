@@ -121,6 +121,8 @@ constexpr int kPromptItemsTarget = 512;    // f32 prompt items a default split a
 constexpr int kGenItemsTarget = 2048;      // f32 generated items a default split aims for
 constexpr int kWideItemsTarget = 512;      // bf16 prompt work groups a default split aims for
 constexpr int kWideMinChunk = 128;         // a default bf16 prompt chunk is at least this long
+constexpr int kWideLongChunk = 256;        // ... and this long when that leaves enough work groups
+constexpr int kWideLongChunkItems = 96;    // prompt work groups the longer chunks must still give
 
 // bf16 items: waves per work group, 16-row MFMA blocks per wave (a wave's
 // output accumulators, RB * D / 4 registers, stay at 32 for D <= 128) and
@@ -264,6 +266,17 @@ inline AttnPlan plan_from_geo(const splice_shape &sh, const splice_call &call, c
     }
     cut(p.geo.n_prompt, prompt_chunk_target(sh), call.split_keys, &p.n_p, &p.p_len,
         bf16_path(sh) ? kWideMinChunk : kMinChunk);
+    if (bf16_path(sh) && call.split_keys == 0) {
+        // chunks of a few tiles spend much of their time starting up and
+        // storing partials: take longer ones when the grid stays wide enough
+        int n_long, len_long;
+        cut(p.geo.n_prompt, prompt_chunk_target(sh), 0, &n_long, &len_long, kWideLongChunk);
+        const int64_t groups = (int64_t)sh.n_kv_heads * row_groups(sh, n_clean, n_active);
+        if (n_long < p.n_p && n_long * groups >= kWideLongChunkItems) {
+            p.n_p = n_long;
+            p.p_len = len_long;
+        }
+    }
     if (bf16_path(sh)) {
         // one generated-row partial per (cell, KV head)
         p.n_g = 1;

@@ -254,20 +254,25 @@ __device__ __forceinline__ void tile_compute(const u32x4_t (&kr)[WaveMfma<D>::ND
     static_for<0, W::NDS>([&](auto st) {
         s = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, kr[st]), qb[st], s, 0, 0, 0);
     });
+    // raw q.k; the scale (> 0) enters the maximum once and each weight's
+    // exponent as one fma
     float x[4];
     float mt = -INFINITY;
     static_for<0, 4>([&](auto i) {
         const int key = 4 * quad + i;
-        x[i] = (col_on && key < n_valid) ? s[(int)i] * qk_scale : -INFINITY;
+        x[i] = (col_on && key < n_valid) ? s[(int)i] : -INFINITY;
         mt = fmaxf(mt, x[i]);
     });
-    mt = fmaxf(mt, __shfl_xor(mt, 16));
-    mt = fmaxf(mt, __shfl_xor(mt, 32));
+    mt *= qk_scale;
     // lazy rescale: a column moves its maximum only when a score exceeds it
-    // by more than kSlack (weights stay <= 2^kSlack); every lane of a column
-    // takes the same decision, and other columns multiply by exactly 1
-    const bool need = mt > S.m + kSlack;
-    if (__any(need)) {
+    // by more than kSlack (weights stay <= 2^kSlack).  Each lane checks its
+    // own scores first; only then are the column's four lanes combined, so
+    // that every lane of a column takes the same decision (other columns
+    // multiply by exactly 1)
+    if (__any(mt > S.m + kSlack)) {
+        mt = fmaxf(mt, __shfl_xor(mt, 16));
+        mt = fmaxf(mt, __shfl_xor(mt, 32));
+        const bool need = mt > S.m + kSlack;
         const float mn = need ? fmaxf(S.m, mt) : S.m;
         const float al = need ? fast_exp2(S.m - (mn == -INFINITY ? 0.f : mn)) : 1.f;
         S.lsum *= al;
@@ -277,7 +282,7 @@ __device__ __forceinline__ void tile_compute(const u32x4_t (&kr)[WaveMfma<D>::ND
     const float ms = S.m == -INFINITY ? 0.f : S.m;
     i16x4_t pb;
     static_for<0, 4>([&](auto i) {
-        const float p = fast_exp2(x[i] - ms);
+        const float p = fast_exp2(fmaf(x[i], qk_scale, -ms));
         S.lsum += p;
         pb[(int)i] = __builtin_bit_cast(short, (__bf16)p);
     });
