@@ -650,7 +650,7 @@ __device__ int fused_prompt_item(const AttnArgs &a, int item, char *lds, int *s_
     const int g = u / a.n_p, pk = u % a.n_p;
     const int lane = threadIdx.x & 63, col = lane & 15, quad = lane >> 4;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-    bf16x8_t qb[RB][X::NDS];
+    const char *qrow[RB];
     int cell[RB], hh[RB], lo[RB];
     bool ok[RB];
     // row groups of unspliced cells come first; a group never mixes classes
@@ -665,8 +665,7 @@ __device__ int fused_prompt_item(const AttnArgs &a, int item, char *lds, int *s_
         cell[rb] = ok[rb] ? a.order[cidx] : 0;
         hh[rb] = R % G;
         lo[rb] = a.row_lo && ok[rb] ? cell_geo(a, cell[rb]).jp0 : 0;
-        load_q_cols<D>(ok[rb] ? a.q + ((size_t)cell[rb] * a.Hq + (size_t)g * G + hh[rb]) * X::ROW : nullptr,
-                       qb[rb]);
+        qrow[rb] = ok[rb] ? a.q + ((size_t)cell[rb] * a.Hq + (size_t)g * G + hh[rb]) * X::ROW : nullptr;
     });
 
     // the prompt chunk: clean before and after the span; the span from the
@@ -694,7 +693,7 @@ __device__ int fused_prompt_item(const AttnArgs &a, int item, char *lds, int *s_
         S.m[rb] = -INFINITY;
         S.lsum[rb] = 0.f;
     });
-    direct_stream<D, RB, Fused<D>::NW>(L, qb, a.qk_scale, a.row_lo != 0, lo, lds, S);
+    direct_stream<D, RB, Fused<D>::NW>(L, qrow, a.qk_scale, a.row_lo != 0, lo, lds, S);
 
     const __amdgpu_buffer_rsrc_t r = part_rsrc(a);
     static_for<0, RB>([&](auto rb) {
@@ -724,9 +723,104 @@ __device__ int fused_prompt_item(const AttnArgs &a, int item, char *lds, int *s_
     return g;
 }
 
+// In-place merge of a generated-row item whose cells' prompt partials are
+// all stored: the item's own partial (its waves combined through LDS) is
+// the last slot and never leaves the chip.  Each thread owns up to U units
+// (cell, q head, four outputs) per round; the loads of every prompt slot of
+// a round's units are issued before the waves' partials are combined, so
+// their latency overlaps the LDS work.  Fold order (fixed, as in
+// combine_cells): the ZERO term, the prompt slots in order, this item's
+// slot.
+template <int D, int G, int NW, int B, int U>
+__device__ __forceinline__ void gen_merge_in_place(const AttnArgs &a, const WaveState<D> &S, char *buf, int wpp,
+                                                   int n_pairs, int c0, int g) {
+    using W = WaveMfma<D>;
+    constexpr int NT = NW * 64;
+    constexpr int UPG = G * D / 4;   // units of four outputs per (cell, KV head)
+    const __amdgpu_buffer_rsrc_t r = part_rsrc(a);
+    const uint32_t slot_bytes = (uint32_t)a.slot_floats * 4u;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int col = lane & 15, quad = lane >> 4;
+    const int total = n_pairs * UPG;
+    float *s_o = reinterpret_cast<float *>(buf);   // [NW][G][D]
+    float *s_m = s_o + NW * G * D;                  // [NW][G]
+    float *s_l = s_m + NW * G;                      // [NW][G]
+    // the waves' partials into LDS (every wave is done with its V^T tile)
+    if (col < G) {
+        static_for<0, W::NDT>([&](auto t) {
+            *reinterpret_cast<f32x4_t *>(s_o + (wave * G + col) * D + 16 * t + 4 * quad) = S.o[t];
+        });
+        if (quad == 0) {
+            s_m[wave * G + col] = S.m;
+            s_l[wave * G + col] = S.lsum;
+        }
+    }
+    for (int e0 = 0; e0 < total; e0 += NT * U) {
+        f32x4_t ok[U][B];
+        float mk[U][B], lk[U][B];
+        int pe[U], he[U], de[U];
+        static_for<0, U>([&](auto u) {
+            const int e = min(e0 + (int)u * NT + tid, total - 1);   // past the end: repeat a valid unit
+            pe[u] = e / UPG;
+            he[u] = (e % UPG) / (D / 4);
+            de[u] = 4 * (e % (D / 4));
+            const uint32_t sbase = slot_off(a, c0 + pe[u], g, 0);
+            const uint32_t o_off = (uint32_t)(he[u] * D + de[u]) * 4u;
+            const uint32_t m_off = (uint32_t)(G * D + he[u]) * 4u, l_off = (uint32_t)(G * D + G + he[u]) * 4u;
+#pragma unroll
+            for (int j = 0; j < B; ++j) {
+                if (j < a.n_p) {
+                    const uint32_t off = sbase + (uint32_t)j * slot_bytes;
+                    ok[u][j] = part_load4(r, off + o_off);
+                    mk[u][j] = part_load1(r, off + m_off);
+                    lk[u][j] = part_load1(r, off + l_off);
+                }
+            }
+        });
+        __syncthreads();   // the staged partials are visible (first round); no-op ordering after
+        static_for<0, U>([&](auto u) {
+            const int e = e0 + (int)u * NT + tid;
+            const int cq = c0 + pe[u];
+            if (e < total && cell_active(a, cq)) {
+                const int h = he[u], d = de[u], w0 = pe[u] * wpp;
+                // this item's partial: its waves combined
+                float Mg = -INFINITY;
+#pragma unroll
+                for (int i = 0; i < NW; ++i)
+                    if (i < wpp) Mg = fmaxf(Mg, s_m[(w0 + i) * G + h]);
+                const float Mgs = Mg == -INFINITY ? 0.f : Mg;
+                float Lg = 0.f;
+                f32x4_t Og = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                for (int i = 0; i < NW; ++i) {
+                    if (i < wpp) {
+                        const int w = w0 + i;
+                        const float f = fast_exp2(s_m[w * G + h] - Mgs);
+                        Lg = fmaf(s_l[w * G + h], f, Lg);
+                        Og += *reinterpret_cast<const f32x4_t *>(s_o + (w * G + h) * D + d) * f;
+                    }
+                }
+                const int nz = zero_slots(a, cq);
+                float M = nz > 0 ? 0.f : -INFINITY;
+#pragma unroll
+                for (int j = 0; j < B; ++j)
+                    if (j < a.n_p) M = fmaxf(M, mk[u][j]);
+                M = fmaxf(M, Mg);
+                float Ls = nz > 0 ? (float)nz * fast_exp2(-M) : 0.f;
+                f32x4_t O = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                for (int j = 0; j < B; ++j)
+                    if (j < a.n_p) fold_slot(mk[u][j], lk[u][j], ok[u][j], M, Ls, O);
+                fold_slot(Mg, Lg, Og, M, Ls, O);   // this item's slot, a.n_p, comes last
+                write_row(a, cq * a.Hq + g * G + h, d, D, M, Ls, O);
+            }
+        });
+    }
+}
+
 // Generated-row item: KV head g and P = a.gen_pairs consecutive cells, wpp =
 // NW / P waves per (cell, KV head) pair streaming that cell's generated rows
-// (interleaved tiles).  After streaming, thread 0 polls the pairs' counters
+// (interleaved tiles).  After streaming, the first wave polls the pairs' counters (a lane per pair)
 // until every prompt chunk has stored its partial (at most a.wait_polls polls
 // in all; prompt items have lower block indices and never wait, so they are
 // dispatched first and finish).  Then this item merges in place: its own
@@ -784,29 +878,31 @@ __device__ int fused_gen_item(const AttnArgs &a, int item, char *lds, int *s_lis
                                                                      lds + wave * W::LDS, S);
     state_finish(S);
 
-    if (threadIdx.x == 0) {
-        bool ready = true;
-        int polls = 0;
-        for (int q = 0; q < n_pairs && ready; ++q) {
-            if (!cell_active(a, c0 + q)) continue;
-            const int *cnt = a.counters + (c0 + q) * a.Hkv + g;
-            bool done = a.n_p == 0;
-            while (!done && polls < a.wait_polls) {
-                done = __hip_atomic_load(cnt, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) >= a.n_p;
-                if (!done) {
-                    __builtin_amdgcn_s_sleep(4);
-                    ++polls;
-                }
-            }
-            ready = done;
+    if (threadIdx.x < 64) {   // wave 0: lane q polls the counter of pair q, all pairs at once
+        const int lane = threadIdx.x;
+        const bool mine = lane < n_pairs && a.n_p > 0 && cell_active(a, c0 + lane);
+        const int *cnt = a.counters + (c0 + (mine ? lane : 0)) * a.Hkv + g;
+        bool done = !mine;
+        int polls = 0;   // the same in every lane
+        while (true) {
+            if (!done) done = __hip_atomic_load(cnt, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) >= a.n_p;
+            if (__all(done) || polls >= a.wait_polls) break;
+            __builtin_amdgcn_s_sleep(4);
+            ++polls;
         }
-        s_list[0] = ready ? -1 : 0;
+        const bool ready = __all(done);
+        if (lane == 0) s_list[0] = ready ? -1 : 0;
     }
     __syncthreads();   // also: every wave is done with its V^T tile
     const bool ready = s_list[0] < 0;
     const __amdgpu_buffer_rsrc_t r = part_rsrc(a);
     const uint32_t slot_bytes = (uint32_t)a.slot_floats * 4u;
     if (ready) {
+        if (a.n_p <= 8) {
+            gen_merge_in_place<D, G, NW, 8, 2>(a, S, lds, wpp, n_pairs, c0, g);
+        } else if (a.n_p <= 16) {
+            gen_merge_in_place<D, G, NW, 16, 1>(a, S, lds, wpp, n_pairs, c0, g);
+        } else {
         waves_merge<D, G, NW>(S, lds, wpp, n_pairs, [&](int q, int h, int d, float Mg, float Lg, f32x4_t Og) {
             const int cq = c0 + q;
             if (!cell_active(a, cq)) return;
@@ -844,6 +940,7 @@ __device__ int fused_gen_item(const AttnArgs &a, int item, char *lds, int *s_lis
             fold_slot(Mg, Lg, Og, M, Ls, O);   // this item's slot, a.n_p, comes last
             write_row(a, cq * a.Hq + g * G + h, d, D, M, Ls, O);
         });
+        }
         if ((int)threadIdx.x < n_pairs && cell_active(a, c0 + threadIdx.x))
             __hip_atomic_store(a.counters + (c0 + threadIdx.x) * a.Hkv + g, 0, __ATOMIC_RELAXED,
                                __HIP_MEMORY_SCOPE_AGENT);

@@ -301,18 +301,13 @@ __device__ __forceinline__ TileRef iter_next(const KeyList &L, TileIter &it, int
 // empty one past the end), so the count of loads in flight is the same in
 // every iteration and one vmcnt wait finds tile t complete.
 template <int D, int RB, int NW>
-__device__ __forceinline__ void direct_stream(const KeyList &L, const bf16x8_t (&qb)[RB][D / 32],
-                                              float qk_scale, bool row_lo, const int (&lo)[RB], char *lds,
-                                              WideState<D, RB> &S) {
+__device__ __forceinline__ void direct_stream(const KeyList &L, const char *const (&qrow)[RB], float qk_scale,
+                                              bool row_lo, const int (&lo)[RB], char *lds, WideState<D, RB> &S) {
     using X = Direct<D>;
     constexpr int NB = X::NB;
     constexpr int LPT = direct_loads_per_thread<D, NW>();
     const int n_tiles = list_tiles(L);
     if (n_tiles == 0) return;
-    // the compiler's own loads (q) are complete before the ring starts: a
-    // wait it would otherwise place inside the loop, before their first use,
-    // would also wait for the tiles in flight
-    wait_vmcnt<0>();
     const DirectLanes<D, NW> dl = direct_lanes<D, NW>();
     const uint32_t lds0 = (uint32_t)__builtin_amdgcn_readfirstlane((int)lds_offset(lds));
     TileIter it;
@@ -326,6 +321,13 @@ __device__ __forceinline__ void direct_stream(const KeyList &L, const bf16x8_t (
         ref[i] = iter_next<X::TK>(L, it, X::ROW);
         direct_issue<D, NW>(ref[i], lds0 + i * X::BUF, dl);
     });
+    // q (the rows' MFMA operands; a NULL row reads zeros) is loaded while the
+    // first tiles are in flight, and the ring starts once both are in: the
+    // compiler, which does not see the tile loads, places no wait of its own
+    // inside the loop after this one
+    bf16x8_t qb[RB][X::NDS];
+    static_for<0, RB>([&](auto rb) { load_q_cols<D>(qrow[rb], qb[rb]); });
+    wait_vmcnt<0>();
     for (int base = 0; base < n_tiles; base += NB) {
         static_for<0, NB>([&](auto j) {
             constexpr int jj = decltype(j)::value;
