@@ -58,7 +58,7 @@ extern "C" {
 #define SPLICE_API
 #endif
 
-#define SPLICE_ABI_VERSION 3
+#define SPLICE_ABI_VERSION 4
 #define SPLICE_MAX_CELLS 256
 
 typedef enum {
@@ -205,6 +205,36 @@ SPLICE_API int32_t splice_decode_step(const splice_shape *shape, const splice_ca
                            const void *clean_k, const void *clean_v,
                            const void *donor_k, const void *donor_v,
                            void *gen_k, void *gen_v,
+                           float *out, float *lse,
+                           void *workspace, size_t workspace_bytes,
+                           void *stream);
+
+/*
+ * The attention of a forked sweep at one (layer, step) (Section 3: a cell
+ * (L, W) is the clean run until step W -- nothing is spliced before it --
+ * so the clean run is decoded once and each cell forks from it at its onset
+ * W).  Cell `trunk` is the clean run: it must never be spliced
+ * (L_trunk >= n_layers).  Cell c has diverged from the trunk at call->step
+ * iff c == trunk, or L_c < n_layers and call->step >= W_c.
+ *   diverged c   attends exactly as splice_decode_attn, except that its
+ *                generated rows below W_c are read from the trunk's
+ *                generated caches (gen_k, gen_v of cell trunk) and its
+ *                rows W_c .. step from its own; its own rows below W_c
+ *                are never read (the trunk reads all of its own rows);
+ *   other cells  are the clean run at this step: out[c], lse[c] are
+ *                written with the trunk's values, bit for bit, and q[c]
+ *                and their caches are not read.
+ * bf16 only (f32: SPLICE_EUNSUPPORTED).  Errors as splice_decode_attn, plus
+ * SPLICE_EINVAL for a negative trunk (with n_cells > 0) and SPLICE_ESHAPE
+ * for trunk >= n_cells or a trunk that some layer splices.  Workspace as
+ * splice_decode_attn.
+ */
+SPLICE_API int32_t splice_decode_forked(const splice_shape *shape, const splice_call *call,
+                           const int32_t *cell_LW, int32_t trunk,
+                           const void *q,
+                           const void *clean_k, const void *clean_v,
+                           const void *donor_k, const void *donor_v,
+                           const void *gen_k, const void *gen_v,
                            float *out, float *lse,
                            void *workspace, size_t workspace_bytes,
                            void *stream);

@@ -32,6 +32,9 @@ struct AttnArgs {
     int row_lo;       // prompt items mask the keys before each row's first visible slot
     const char *kn, *vn;   // bf16 decode step: the current token's K, V [C][Hkv][D], appended
     int32_t cstep[SPLICE_MAX_CELLS];
+    int trunk;        // forked sweep: the cell of the clean run (-1: none); see fused_gen_item
+    int n_dormant;    // forked sweep: cells not yet diverged, order[n_active ..], given the trunk's result
+    int32_t wfork[SPLICE_MAX_CELLS];   // forked sweep: a cell's generated rows below wfork are the trunk's
     int gen_pairs;    // bf16 generated-row items: (cell, KV head) pairs per work group
     int gen_v_nt;     // bf16 generated-row items: V rows loaded non-temporally
     float qk_scale;   // scale * log2(e)
@@ -421,9 +424,23 @@ __device__ __forceinline__ int zero_slots(const AttnArgs &a, int c) {
 
 __device__ __forceinline__ bool has_zero_term(const AttnArgs &a, int c) { return zero_slots(a, c) > 0; }
 
-__device__ __forceinline__ void write_row(const AttnArgs &a, int row, int d, int D, float M, float L, f32x4_t O) {
-    *reinterpret_cast<f32x4_t *>(a.out + (size_t)row * D + d) = O * (1.f / L);
-    if (d == 0) a.lse[row] = (M + log2f(L)) * kLn2;
+// Output row (cell c, q head hq): four outputs at d, and lse.  Under a forked
+// sweep the trunk's rows are also the rows of every cell that has not yet
+// diverged from it.
+__device__ __forceinline__ void write_row(const AttnArgs &a, int c, int hq, int d, int D, float M, float L,
+                                          f32x4_t O) {
+    const f32x4_t o = O * (1.f / L);
+    const float lse = (M + log2f(L)) * kLn2;
+    const size_t row = (size_t)c * a.Hq + hq;
+    *reinterpret_cast<f32x4_t *>(a.out + row * D + d) = o;
+    if (d == 0) a.lse[row] = lse;
+    if (c == a.trunk) {
+        for (int i = 0; i < a.n_dormant; ++i) {
+            const size_t r2 = (size_t)a.order[a.n_active + i] * a.Hq + hq;
+            *reinterpret_cast<f32x4_t *>(a.out + r2 * D + d) = o;
+            if (d == 0) a.lse[r2] = lse;
+        }
+    }
 }
 
 // Merge the partial results of cells list[0..n) of KV head g.  One round of
@@ -496,7 +513,7 @@ __device__ void combine_cells(const AttnArgs &a, const int *list, int n, int g, 
             if (u < total) {
                 const int i = u / UPC, rem = u % UPC;
                 const int h = rem / (D / 4), d = 4 * (rem % (D / 4));
-                write_row(a, list[i] * a.Hq + g * G + h, d, D, M[b], L[b], O[b]);
+                write_row(a, list[i], g * G + h, d, D, M[b], L[b], O[b]);
             }
         }
     }
@@ -812,7 +829,7 @@ __device__ __forceinline__ void gen_merge_in_place(const AttnArgs &a, const Wave
                 for (int j = 0; j < B; ++j)
                     if (j < a.n_p) fold_slot(mk[u][j], lk[u][j], ok[u][j], M, Ls, O);
                 fold_slot(Mg, Lg, Og, M, Ls, O);   // this item's slot, a.n_p, comes last
-                write_row(a, cq * a.Hq + g * G + h, d, D, M, Ls, O);
+                write_row(a, cq, g * G + h, d, D, M, Ls, O);
             }
         });
     }
@@ -863,6 +880,13 @@ __device__ int fused_gen_item(const AttnArgs &a, int item, char *lds, int *s_lis
             list_add(L, a.gk + goff, a.gv + goff, geo.n_gen - 1);
             const size_t noff = ((size_t)c * a.Hkv + g) * W::ROW;
             list_add(L, a.kn + noff, a.vn + noff, 1);
+        } else if (a.trunk >= 0 && c != a.trunk) {
+            // forked sweep: rows below the fork step are the trunk's, the rest the cell's own
+            const int i1 = geo.i0 + geo.n_gen, wf = min(max(a.wfork[c], geo.i0), i1);
+            const size_t toff = (((size_t)a.trunk * a.Hkv + g) * (size_t)a.cap + geo.i0) * W::ROW;
+            list_add(L, a.gk + toff, a.gv + toff, wf - geo.i0);
+            const size_t ooff = (((size_t)c * a.Hkv + g) * (size_t)a.cap + wf) * W::ROW;
+            list_add(L, a.gk + ooff, a.gv + ooff, i1 - wf);
         } else {
             list_add(L, a.gk + goff, a.gv + goff, geo.n_gen);
         }
@@ -938,7 +962,7 @@ __device__ int fused_gen_item(const AttnArgs &a, int item, char *lds, int *s_lis
                 }
             }
             fold_slot(Mg, Lg, Og, M, Ls, O);   // this item's slot, a.n_p, comes last
-            write_row(a, cq * a.Hq + g * G + h, d, D, M, Ls, O);
+            write_row(a, cq, g * G + h, d, D, M, Ls, O);
         });
         }
         if ((int)threadIdx.x < n_pairs && cell_active(a, c0 + threadIdx.x))

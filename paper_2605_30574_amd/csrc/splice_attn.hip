@@ -231,10 +231,12 @@ int32_t splice_workspace_init(void *workspace, size_t workspace_bytes, void *str
 
 namespace {
 
-// splice_decode_attn (cell_step == nullptr: every cell at call->step) and
-// splice_decode_step (each cell at cell_step[c], k_new/v_new appended).
+// splice_decode_attn (cell_step == nullptr, trunk < 0: every cell at
+// call->step), splice_decode_step (each cell at cell_step[c], k_new/v_new
+// appended) and splice_decode_forked (trunk >= 0: cells that have not
+// diverged from the trunk by call->step take its result).
 int32_t decode_attn_impl(const splice_shape *shape, const splice_call *call, const int32_t *cell_LW,
-                         const int32_t *cell_step, const void *q, const void *k_new, const void *v_new,
+                         const int32_t *cell_step, int trunk, const void *q, const void *k_new, const void *v_new,
                          const void *clean_k, const void *clean_v, const void *donor_k, const void *donor_v,
                          const void *gen_k, const void *gen_v, float *out, float *lse, void *workspace,
                          size_t workspace_bytes, void *stream) {
@@ -266,10 +268,20 @@ int32_t decode_attn_impl(const splice_shape *shape, const splice_call *call, con
     if (!zero && (!splice::aligned(donor_k, 16) || !splice::aligned(donor_v, 16))) return SPLICE_EINVAL;
     if (!splice::aligned(out, 16) || !splice::aligned(lse, 4)) return SPLICE_EINVAL;
     if (ragged && (!splice::aligned(k_new, 16) || !splice::aligned(v_new, 16))) return SPLICE_EINVAL;
-    if (ragged && !splice::bf16_path(sh)) return SPLICE_EUNSUPPORTED;
+    const bool forked = trunk >= 0;
+    if (forked && (trunk >= sh.n_cells || cell_LW[2 * trunk] < sh.n_layers)) return SPLICE_ESHAPE;
+    if ((ragged || forked) && !splice::bf16_path(sh)) return SPLICE_EUNSUPPORTED;
 
-    // the steps of the call: one for every cell, or each cell's own
-    auto step_of = [&](int c) { return ragged ? cell_step[c] : call->step; };
+    // a forked sweep's cell has diverged from the trunk once it has been
+    // spliced at some layer, i.e. from step W_c on if L_c < n_layers
+    auto diverged = [&](int c) {
+        return c == trunk || (cell_LW[2 * c] < sh.n_layers && call->step >= cell_LW[2 * c + 1]);
+    };
+    // the steps of the call: one for every cell, each cell's own, or (forked)
+    // the call's for diverged cells and none for the others
+    auto step_of = [&](int c) {
+        return ragged ? cell_step[c] : (forked && !diverged(c) ? -1 : call->step);
+    };
     int s_min = INT32_MAX, s_max = -1, n_active = 0;
     for (int c = 0; c < sh.n_cells; ++c) {
         const int s = step_of(c);
@@ -335,7 +347,8 @@ int32_t decode_attn_impl(const splice_shape *shape, const splice_call *call, con
     a.gen_v_nt = splice::gen_v_nontemporal(sh) ? 1 : 0;
     a.wait_polls = call->merge_wait == 0 ? kDefaultWaitPolls : (call->merge_wait < 0 ? 0 : call->merge_wait);
     a.qk_scale = call->scale * kLog2e;
-    a.ragged = ragged ? 1 : 0;
+    a.ragged = ragged || forked ? 1 : 0;
+    a.trunk = forked ? trunk : -1;
     a.window = call->window;
     a.span_lo = sh.span_lo; a.span_hi = sh.span_hi;
     a.row_lo = ragged && g_lo.jp0 != g_hi.jp0 ? 1 : 0;
@@ -349,6 +362,13 @@ int32_t decode_attn_impl(const splice_shape *shape, const splice_call *call, con
     for (int c = 0; c < sh.n_cells; ++c)
         if (step_of(c) >= 0 && (spliced[c >> 5] >> (c & 31) & 1u)) a.order[n++] = (uint8_t)c;
     a.n_active = n;
+    a.n_dormant = 0;
+    if (forked) {   // then the cells that take the trunk's result
+        for (int c = 0; c < sh.n_cells; ++c)
+            if (step_of(c) < 0) a.order[n++] = (uint8_t)c;
+        a.n_dormant = n - a.n_active;
+    }
+    for (int c = 0; c < SPLICE_MAX_CELLS; ++c) a.wfork[c] = forked && c < sh.n_cells ? cell_LW[2 * c + 1] : 0;
     for (; n < SPLICE_MAX_CELLS; ++n) a.order[n] = 0;
     if (splice::bf16_path(sh)) {
         a.n_rb = splice::row_groups(sh, a.n_clean, a.n_active);
@@ -376,7 +396,7 @@ int32_t splice_decode_attn(const splice_shape *shape, const splice_call *call, c
                            const void *donor_k, const void *donor_v, const void *gen_k,
                            const void *gen_v, float *out, float *lse, void *workspace,
                            size_t workspace_bytes, void *stream) {
-    return decode_attn_impl(shape, call, cell_LW, nullptr, q, nullptr, nullptr, clean_k, clean_v, donor_k,
+    return decode_attn_impl(shape, call, cell_LW, nullptr, -1, q, nullptr, nullptr, clean_k, clean_v, donor_k,
                             donor_v, gen_k, gen_v, out, lse, workspace, workspace_bytes, stream);
 }
 
@@ -386,7 +406,17 @@ int32_t splice_decode_step(const splice_shape *shape, const splice_call *call, c
                            const void *donor_v, void *gen_k, void *gen_v, float *out, float *lse,
                            void *workspace, size_t workspace_bytes, void *stream) {
     if (!cell_step && shape && shape->n_cells > 0) return SPLICE_EINVAL;
-    return decode_attn_impl(shape, call, cell_LW, cell_step, q, k_new, v_new, clean_k, clean_v, donor_k,
+    return decode_attn_impl(shape, call, cell_LW, cell_step, -1, q, k_new, v_new, clean_k, clean_v, donor_k,
+                            donor_v, gen_k, gen_v, out, lse, workspace, workspace_bytes, stream);
+}
+
+int32_t splice_decode_forked(const splice_shape *shape, const splice_call *call, const int32_t *cell_LW,
+                             int32_t trunk, const void *q, const void *clean_k, const void *clean_v,
+                             const void *donor_k, const void *donor_v, const void *gen_k, const void *gen_v,
+                             float *out, float *lse, void *workspace, size_t workspace_bytes, void *stream) {
+    if (shape && shape->n_cells > 0 && trunk < 0) return SPLICE_EINVAL;
+    if (shape && shape->n_cells == 0) trunk = -1;
+    return decode_attn_impl(shape, call, cell_LW, nullptr, trunk, q, nullptr, nullptr, clean_k, clean_v, donor_k,
                             donor_v, gen_k, gen_v, out, lse, workspace, workspace_bytes, stream);
 }
 

@@ -25,7 +25,7 @@ def test_library_exports_every_declared_symbol():
     lib = sp.load_library()
     for name in declared:
         assert hasattr(lib, name), name
-    assert sp.splice_abi_version() == 3
+    assert sp.splice_abi_version() == 4
 
 
 def test_single_hip_runtime_mapped():
@@ -178,3 +178,24 @@ def test_decode_step_validation_before_device_access():
     st = (ctypes.c_int32 * 6)(*([0] * 6))
     assert lib.splice_decode_step(ctypes.byref(sh), ctypes.byref(bad), lw, st, fake, fake, fake, fake, fake, None,
                                   None, fake, fake, fake, fake, ws, need, None) == sp.SPLICE_ESHAPE
+
+
+def test_decode_forked_validation_before_device_access():
+    lib = sp.load_library()
+    sh = _shape(dtype="bf16")            # 6 cells, 2 layers
+    call = sp.make_call(1, 5, 0, 0.125)
+    fake = ctypes.c_void_p(0x1000)
+    ws = ctypes.c_void_p(0x2000)
+    need = sp.splice_decode_attn_workspace_bytes(sh)
+
+    def forked(shape, cells, trunk, wbytes=need):
+        lw = (ctypes.c_int32 * (2 * len(cells)))(*[x for c in cells for x in c])
+        return lib.splice_decode_forked(ctypes.byref(shape), ctypes.byref(call), lw, trunk, fake, fake, fake,
+                                        None, None, fake, fake, fake, fake, ws, wbytes, None)
+
+    cells = [(2, 0), (0, 0), (1, 4), (0, 9), (1, 1), (2, 3)]   # cells 0 and 5 are never spliced (L >= 2)
+    assert forked(sh, cells, -1) == sp.SPLICE_EINVAL           # a trunk is required
+    assert forked(sh, cells, 6) == sp.SPLICE_ESHAPE            # out of range
+    assert forked(sh, cells, 1) == sp.SPLICE_ESHAPE            # the trunk would be spliced
+    assert forked(sh, cells, 0, wbytes=16) == sp.SPLICE_EWORKSPACE
+    assert forked(_shape(dtype="f32"), cells, 0) == sp.SPLICE_EUNSUPPORTED
