@@ -24,6 +24,11 @@ Reported (one JSON line):
               (else null);
   cpu_baseline  the fp64 oracle timed on this host's cores on a stratified
               sample of the same workload's calls;
+  forked      the same sweep through splice_decode_forked (one clean run,
+              each cell forked from it at its onset W; a never-spliced cell
+              of the grid is the trunk): ms per step, cell-steps/s, GB/s of
+              its algorithmic bytes, the fraction of cell-steps computed,
+              and the speed-up over the lock-step region;
   decode_step  splice_decode_step passes (each cell at its own step, the
               current token's K/V appended, finished cells skipped) over two
               seeded step mixes -- 1/8 and 1/2 of the cells finished --
@@ -129,6 +134,36 @@ def step_bytes(w, layer: int, steps, cells) -> int:
     return total
 
 
+def forked_bytes(w, layer: int, step: int, cells, trunk: int) -> int:
+    """Bytes a splice_decode_forked call must move at minimum: the prompt as
+    in call_bytes for the diverged cells, the trunk's visible generated rows
+    once (its own and, below their onsets, the forked cells'), each diverged
+    cell's own rows from its onset on, q of the diverged cells, out and lse
+    of every cell."""
+    e = w.elem_bytes
+    row = 2 * w.n_kv_heads * w.head_dim * e
+    Tp, (a, b) = w.prompt_len, w.span
+    win = w.window(layer)
+    p = Tp + step
+    j0 = p - win + 1 if win > 0 else 0
+    jp0 = min(max(j0, 0), Tp)
+    i0 = max(0, j0 - Tp)
+    sa = min(max(a, jp0), Tp)
+    sb = min(max(b, sa), Tp)
+    n_sv, n_ns = sb - sa, (Tp - jp0) - (sb - sa)
+    N = w.n_layers
+    div = [c for c, (L, W) in enumerate(cells) if c == trunk or (L < N and step >= W)]
+    spl = [layer >= cells[c][0] and step >= cells[c][1] for c in div]
+    total = n_ns * row
+    total += n_sv * row if not all(spl) else 0
+    total += n_sv * row if any(spl) and w.donor != "zero" else 0
+    total += (step + 1 - i0) * row                                       # the trunk's rows
+    total += sum(max(0, step + 1 - max(i0, cells[c][1])) for c in div if c != trunk) * row
+    total += len(div) * w.n_q_heads * w.head_dim * e
+    total += len(cells) * w.n_q_heads * (4 * w.head_dim + 4)
+    return total
+
+
 def launch_kernels(w) -> str:
     """The kernel one splice_decode_attn call launches on this workload: bf16
     calls launch the one kernel of shared-prompt and generated-row items."""
@@ -223,6 +258,7 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=20.0)
     ap.add_argument("--eager", action="store_true", help="launch without graphs")
+    ap.add_argument("--no-forked", action="store_true", help="skip the forked-sweep measurement")
     ap.add_argument("--copy-calibration", type=int, default=0,
                     help="only run a plain device copy of this many MiB (counter calibration)")
     args = ap.parse_args()
@@ -385,6 +421,55 @@ def main():
         log("decode passes: " + ", ".join(f"{k}: {v['us_per_launch']} us/launch, {v['GB/s']} GB/s, "
                                            f"{v['active_cells']} active" for k, v in decode_step.items()))
 
+    # the same sweep decoded as one clean run that the cells fork from at
+    # their onsets (splice_decode_forked), when the grid has a never-spliced
+    # cell to be the trunk; timed after the main region, graph per step
+    forked = None
+    never = [c for c, (L, W) in enumerate(w.cells) if L >= N]
+    if w.dtype == "bf16" and never and not args.no_forked:
+        trunk = never[0]
+        cells = list(w.cells)
+
+        def issue_forked(s: int):
+            for l in range(N):
+                b = layers[l]
+                sp.splice_decode_forked(shape, sp.make_call(l, s, w.window(l), w.scale), lw, trunk, qs[l],
+                                        b["clean_k"], b["clean_v"], b["donor_k"], b["donor_v"],
+                                        b["gen_k"], b["gen_v"], out, lse, ws)
+        fgraphs = {}
+        if not args.eager:
+            for s in sorted(set(timed_steps) | set(warm_steps)):
+                g = torch.cuda.CUDAGraph()
+                with torch.cuda.graph(g, stream=stream):
+                    issue_forked(s)
+                fgraphs[s] = g
+
+        def run_forked(steps_list):
+            with torch.cuda.stream(stream):
+                for s in steps_list:
+                    if args.eager:
+                        issue_forked(s)
+                    else:
+                        fgraphs[s].replay()
+        run_forked(warm_steps)
+        torch.cuda.synchronize()
+        f0 = torch.cuda.Event(enable_timing=True)
+        f1 = torch.cuda.Event(enable_timing=True)
+        f0.record(stream)
+        run_forked(timed_steps)
+        f1.record(stream)
+        torch.cuda.synchronize()
+        fsec = f0.elapsed_time(f1) / 1e3
+        fbytes = sum(forked_bytes(w, l, s, cells, trunk) for s in timed_steps for l in range(N))
+        n_div = [sum(1 for c, (L, W) in enumerate(cells) if c == trunk or (L < N and s >= W)) for s in timed_steps]
+        forked = {"trunk_cell": list(cells[trunk]), "ms_per_step": round(fsec * 1e3 / K, 4),
+                  "cell_steps_per_s": round(C * K / fsec, 1), "GB/s": round(fbytes / fsec / 1e9, 1),
+                  "computed_cells_frac": round(sum(n_div) / (C * K), 4),
+                  "speedup_vs_lockstep": round(sec / fsec, 3)}
+        del fgraphs
+        log(f"forked sweep: {forked['ms_per_step']} ms/step, {forked['cell_steps_per_s']} cell-steps/s, "
+            f"{forked['computed_cells_frac']:.3f} of the cell-steps computed, x{forked['speedup_vs_lockstep']}")
+
     traffic, traffic_src = stored_traffic(w.name)
     per_launch_bytes = alg_bytes / launches
     avg_launch_s = sec / launches
@@ -418,6 +503,7 @@ def main():
         "cpu_baseline": cpu,
         "per_step": per_step,
         "decode_step": decode_step,
+        "forked": forked,
     }
     print(json.dumps(res), flush=True)
 
