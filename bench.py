@@ -16,6 +16,9 @@ Reported (one JSON line):
   cell_steps_per_s   C * K / wall time;
   per_step    time per launch and GB/s of one step's N launches at
               s = 0, S/4, S/2, S - 1 (measured after the timed region);
+  per_step_cold  the same steps with the last-level cache flushed before
+              each launch (a 512 MiB read outside the timed events; eager
+              launches, so each includes its dispatch);
   roofline    bound "hbm": achieved = algorithmic bytes per call / average
               call duration (HIP events on the launch stream, over the timed
               region; a call is one kernel launch), peak 8000 GB/s,
@@ -378,6 +381,37 @@ def main():
     log("per-step buckets: " + ", ".join(f"s={k}: {v['us_per_launch']} us/launch, {v['GB/s']} GB/s"
                                           for k, v in per_step.items()))
 
+    # the same buckets cold: before every timed launch a 512 MiB buffer is
+    # read (outside the events), which leaves no tile of the call in the
+    # 256 MiB last-level cache -- and no dirty lines either, as after the
+    # weight reads of a model's other layers
+    flush = torch.ones(128 << 20, dtype=torch.float32, device=dev)
+    flush_sum = torch.empty((), dtype=torch.float32, device=dev)
+    with torch.cuda.stream(stream):
+        torch.sum(flush, 0, out=flush_sum)
+    torch.cuda.synchronize()
+    per_step_cold = {}
+    for s in bucket_steps:
+        tot, nb = 0.0, 0
+        for l in range(N):
+            b = layers[l]
+            with torch.cuda.stream(stream):
+                torch.sum(flush, 0, out=flush_sum)
+                e0 = torch.cuda.Event(enable_timing=True)
+                e1 = torch.cuda.Event(enable_timing=True)
+                e0.record(stream)
+                sp.splice_decode_attn(shape, sp.make_call(l, s, w.window(l), w.scale), lw, qs[l],
+                                      b["clean_k"], b["clean_v"], b["donor_k"], b["donor_v"],
+                                      b["gen_k"], b["gen_v"], out, lse, ws)
+                e1.record(stream)
+            torch.cuda.synchronize()
+            tot += e0.elapsed_time(e1) / 1e3
+            nb += call_bytes(w, l, s, spliced_flags(w, l, s))
+        per_step_cold[str(s)] = {"us_per_launch": round(tot / N * 1e6, 2), "GB/s": round(nb / tot / 1e9, 1)}
+    del flush, flush_sum
+    log("per-step buckets, cold: " + ", ".join(f"s={k}: {v['us_per_launch']} us/launch, {v['GB/s']} GB/s"
+                                                for k, v in per_step_cold.items()))
+
     # decode passes with cells at their own steps (splice_decode_step: KV
     # append + attention, finished cells skipped), outside the timed region:
     # one pass = the N layers' launches, graph-captured like the sweep steps
@@ -502,6 +536,7 @@ def main():
         "roofline": roofline,
         "cpu_baseline": cpu,
         "per_step": per_step,
+        "per_step_cold": per_step_cold,
         "decode_step": decode_step,
         "forked": forked,
     }
