@@ -32,6 +32,10 @@ Reported (one JSON line):
               of the grid is the trunk): ms per step, cell-steps/s, GB/s of
               its algorithmic bytes, the fraction of cell-steps computed,
               and the speed-up over the lock-step region;
+  e2e         the decode loop around the attention with a synthetic model
+              (the workload's attention shape, its model's hidden sizes):
+              ms per pass of all N layers plus the argmax, at the bucket
+              steps, cell-steps/s, and the attention's share of a pass;
   decode_step  splice_decode_step passes (each cell at its own step, the
               current token's K/V appended, finished cells skipped) over two
               seeded step mixes -- 1/8 and 1/2 of the cells finished --
@@ -262,6 +266,7 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=20.0)
     ap.add_argument("--eager", action="store_true", help="launch without graphs")
     ap.add_argument("--no-forked", action="store_true", help="skip the forked-sweep measurement")
+    ap.add_argument("--no-e2e", action="store_true", help="skip the decode-loop measurement")
     ap.add_argument("--copy-calibration", type=int, default=0,
                     help="only run a plain device copy of this many MiB (counter calibration)")
     args = ap.parse_args()
@@ -504,6 +509,58 @@ def main():
         log(f"forked sweep: {forked['ms_per_step']} ms/step, {forked['cell_steps_per_s']} cell-steps/s, "
             f"{forked['computed_cells_frac']:.3f} of the cell-steps computed, x{forked['speedup_vs_lockstep']}")
 
+    # the whole decode loop around the attention (Algorithm 1): a synthetic
+    # model of the workload's attention shape and its model's hidden sizes,
+    # one pass = all N layers' projections, norms and MLPs (library GEMMs)
+    # plus this library's KV append + attention, then the argmax; each
+    # pass captured once per starting step and replayed
+    e2e = None
+    from workloads.model import MODELS, make_weights
+    if w.dtype == "bf16" and w.name in MODELS and not args.no_e2e:
+        from paper_2605_30574_amd import decode
+        m = MODELS[w.name]
+        t0 = time.time()
+        wt = make_weights(w, m, dtype=torch.bfloat16, device=dev, draw_on_device=True)
+        torch.cuda.synchronize()
+        n_params = sum(t.numel() for t in (wt["embed"], wt["lm_head"])) + \
+            sum(t.numel() for L in wt["layers"] for t in L.values())
+        log(f"synthetic model: {n_params / 1e9:.2f} B parameters drawn in {time.time() - t0:.1f} s")
+        dec = decode.SweepDecoder(w, m, wt, layers, lw, device=dev)
+        passes = {}
+        for s0 in bucket_steps:
+            steps = np.full(C, s0, dtype=np.int32)
+            pos = dec.positions(steps)
+            tok = torch.full((C,), 1, dtype=torch.long, device=dev)
+            with torch.cuda.stream(stream):
+                dec.step(tok, steps, pos)
+            torch.cuda.synchronize()
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g, stream=stream):
+                dec.step(tok, steps, pos)
+            with torch.cuda.stream(stream):
+                g.replay()
+            reps = 10
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            torch.cuda.synchronize()
+            e0.record(stream)
+            with torch.cuda.stream(stream):
+                for _ in range(reps):
+                    g.replay()
+            e1.record(stream)
+            torch.cuda.synchronize()
+            ms_pass = e0.elapsed_time(e1) / reps
+            att_ms = per_step[str(s0)]["us_per_launch"] * N / 1e3
+            passes[str(s0)] = {"ms_per_pass": round(ms_pass, 3), "cell_steps_per_s": round(C / ms_pass * 1e3, 1),
+                               "attention_share": round(att_ms / ms_pass, 3)}
+            del g
+        e2e = {"model": {"layers": N, "d_model": m.d_model, "d_ff": m.d_ff, "vocab": m.vocab,
+                         "params_B": round(n_params / 1e9, 2), "weights": "synthetic bf16"},
+               "passes": passes}
+        log("decode loop: " + ", ".join(f"s={k}: {v['ms_per_pass']} ms/pass, {v['cell_steps_per_s']} cell-steps/s, "
+                                        f"attention {100 * v['attention_share']:.0f}%" for k, v in passes.items()))
+        del dec, wt
+
     traffic, traffic_src = stored_traffic(w.name)
     per_launch_bytes = alg_bytes / launches
     avg_launch_s = sec / launches
@@ -539,6 +596,7 @@ def main():
         "per_step_cold": per_step_cold,
         "decode_step": decode_step,
         "forked": forked,
+        "e2e": e2e,
     }
     print(json.dumps(res), flush=True)
 
