@@ -303,16 +303,19 @@ inline AttnPlan plan_from_geo(const splice_shape &sh, const splice_call &call, c
     return p;
 }
 
-// bf16: the generated-row items load V non-temporally when the prompt
-// caches a call reads (clean, plus donor when the donor is a buffer) exceed
-// this many bytes; below it the prompt stays cached either way and normal
-// loads measured faster.
+// bf16: the generated-row items load V non-temporally, so that the rows,
+// read once, do not push the shared prompt tiles out of the caches, when
+// the prompt caches a call reads (clean, plus donor when the donor is a
+// buffer) exceed kGenNtPromptBytes or the call streams at least
+// kGenNtRows generated rows per cell; short calls with small prompts
+// measured faster with normal loads.
 constexpr int64_t kGenNtPromptBytes = (int64_t)16 << 20;
+constexpr int kGenNtRows = 128;
 
-inline bool gen_v_nontemporal(const splice_shape &sh) {
+inline bool gen_v_nontemporal(const splice_shape &sh, int n_gen) {
     const int64_t per_cache = (int64_t)sh.prompt_len * sh.n_kv_heads * sh.head_dim * elem_bytes(sh) * 2;
     const int64_t bytes = per_cache * (sh.donor_kind == SPLICE_DONOR_BUFFER ? 2 : 1);
-    return bytes > kGenNtPromptBytes;
+    return bytes > kGenNtPromptBytes || n_gen >= kGenNtRows;
 }
 
 inline AttnPlan plan_attn(const splice_shape &sh, const splice_call &call, int n_clean) {

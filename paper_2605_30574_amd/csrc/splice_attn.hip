@@ -344,7 +344,7 @@ int32_t decode_attn_impl(const splice_shape *shape, const splice_call *call, con
     a.n_rb = 0; a.n_rg_clean = 0;
     a.n_prompt_items = plan.n_prompt_items;
     a.gen_pairs = plan.gen_pairs;
-    a.gen_v_nt = splice::gen_v_nontemporal(sh) ? 1 : 0;
+    a.gen_v_nt = splice::gen_v_nontemporal(sh, geo.n_gen) ? 1 : 0;
     a.wait_polls = call->merge_wait == 0 ? kDefaultWaitPolls : (call->merge_wait < 0 ? 0 : call->merge_wait);
     a.qk_scale = call->scale * kLog2e;
     a.ragged = ragged || forked ? 1 : 0;
