@@ -169,3 +169,49 @@ def test_graph_replay_matches_eager():
             assert torch.equal(outs[k], ref[k][0]) and torch.equal(lses[k], ref[k][1]), (rep, k)
         issue()                                  # eager work between replays
         torch.cuda.synchronize()
+
+
+def test_workspace_reused_across_calls():
+    """One workspace serves a sequence of calls that alternate between the two
+    merge protocols (at most 8 prompt chunks: the generated-row item polls
+    the prompt slots in a bank per (cell, KV head); more: counters and a flat
+    region), change the slot count, hand the merge over (merge_wait < 0) or
+    mix both sites (1), and skip finished cells (a ragged decode step).  Every
+    call must give the bits the same call gives on a fresh workspace: what a
+    call leaves behind (slot data, bank states, counters) never reaches the
+    next one."""
+    w = _w().with_(prompt_len=1100, span=(40, 1060))
+    lw = workloads.cell_lw(w)
+    C = lw.shape[0]
+    layer = 1
+    shape = gc.shape_of(w, n_cells=C)
+    bufs = gc.gpu_layer(w, layer)
+    # sized for the call with the most slots (64-key chunks)
+    shared = sp.new_workspace(shape, sp.make_call(layer, 150, w.window(layer), w.scale, 64))
+    finished = workloads.cell_steps(w, seed=3, n_cells=C, finished=0.25) < 0
+    plan = [  # (split_keys, merge_wait, step, ragged decode step?)
+        (512, 0, 10, False), (64, 0, 150, False), (256, 1, 40, False), (128, -1, 150, False),
+        (0, 0, 60, True), (512, -1, 150, False), (256, 0, 199, False), (64, 1, 3, False),
+        (0, 0, 61, True), (512, 0, 150, False), (128, 0, 20, False), (256, -1, 150, False)]
+    for i, (split, mw, step, ragged) in enumerate(plan):
+        gc.announce(f"workspace reuse call {i}: split={split} wait={mw} step={step} ragged={ragged}")
+        q = workloads.make_q(w, layer, step, device="cuda")
+        if not ragged:
+            got = gc.run_attn(w, layer, step, bufs, q, lw, split=split, ws=shared, shape=shape, merge_wait=mw)
+            want = gc.run_attn(w, layer, step, bufs, q, lw, split=split, shape=shape, merge_wait=mw)
+        else:
+            steps = np.where(finished, -1, step).astype(np.int32)
+            new = workloads.make_new_rows(w, layer, step, device="cuda", n_cells=C)
+            call = sp.make_call(layer, 0, w.window(layer), w.scale, split, mw)
+            res = []
+            for ws in (shared, sp.new_workspace(shape)):
+                out = torch.full((C, w.n_q_heads, w.head_dim), float("nan"), device="cuda")
+                lse = torch.full((C, w.n_q_heads), float("nan"), device="cuda")
+                sp.splice_decode_step(shape, call, lw, steps, q, new["k_new"], new["v_new"], bufs["clean_k"],
+                                      bufs["clean_v"], bufs["donor_k"], bufs["donor_v"], bufs["gen_k"],
+                                      bufs["gen_v"], out, lse, ws)
+                torch.cuda.synchronize()
+                res.append((out.cpu().numpy(), lse.cpu().numpy()))
+            got, want = res
+        assert np.array_equal(got[0], want[0], equal_nan=True), f"call {i}: out"
+        assert np.array_equal(got[1], want[1], equal_nan=True), f"call {i}: lse"
