@@ -76,6 +76,15 @@ class ReferenceDecoder:
         self.osh = make_shape(1, w.n_q_heads, w.n_kv_heads, w.head_dim, w.prompt_len, w.span, w.n_steps,
                               w.donor == "zero", 2)
 
+    def attend(self, l: int, c: int, s: int, q_c: np.ndarray) -> np.ndarray:
+        """Attention output [Hq][D] of cell c at layer l, step s (q_c: bf16
+        bits [Hq][D]) over its spliced prompt and generated rows 0..s."""
+        w, pr = self.w, self.prompts[l]
+        oc, _ = attn(self.osh, l, s, w.window(l), w.head_dim ** -0.5, self.lw[c:c + 1],
+                     np.ascontiguousarray(q_c[None]), pr["clean_k"], pr["clean_v"], pr["donor_k"], pr["donor_v"],
+                     np.ascontiguousarray(self.gen_k[l][c:c + 1]), np.ascontiguousarray(self.gen_v[l][c:c + 1]))
+        return oc[0]
+
     def forward(self, tokens: np.ndarray, steps: np.ndarray) -> np.ndarray:
         """Logits [C][V] of one decode pass (rows of finished cells are not
         meaningful); steps[c] < 0 marks a finished cell."""
@@ -90,17 +99,13 @@ class ReferenceDecoder:
             k = to_bf16_bits(_rope((h @ p["w_k"]).reshape(C, Hkv, D), pos, m.rope_theta))
             v = to_bf16_bits((h @ p["w_v"]).reshape(C, Hkv, D))
             o = np.zeros((C, Hq, D))
-            pr = self.prompts[l]
             for c in range(C):
                 s = int(steps[c])
                 if s < 0:
                     continue
                 self.gen_k[l][c, :, s] = k[c]
                 self.gen_v[l][c, :, s] = v[c]
-                oc, _ = attn(self.osh, l, s, w.window(l), D ** -0.5, self.lw[c:c + 1], np.ascontiguousarray(q[c:c + 1]),
-                             pr["clean_k"], pr["clean_v"], pr["donor_k"], pr["donor_v"],
-                             np.ascontiguousarray(self.gen_k[l][c:c + 1]), np.ascontiguousarray(self.gen_v[l][c:c + 1]))
-                o[c] = oc[0]
+                o[c] = self.attend(l, c, s, q[c])
             x = x + o.reshape(C, Hq * D) @ p["w_o"]
             h2 = _rms_norm(x, p["norm_2"], m.rms_eps)
             x = x + (_silu(h2 @ p["w_gate"]) * (h2 @ p["w_up"])) @ p["w_down"]

@@ -4,32 +4,40 @@ each layer's KV append and attention) against oracle.decoder (float64 on
 the CPU), teacher-forced -- both decode the GPU's tokens, so a near tie
 cannot send the two down different trajectories.
 
-Bar (tiny float32 model; only q, k, v and the caches are bf16 on both
-sides): logits of every active cell within 2e-2 of the oracle's, relative
-to the largest logit magnitude.  The kernel rounds the softmax weights to
-bf16 for p.v (a reading of the paper, within its attention bar), which moves
-attention outputs by up to ~1e-3 of |v|; two random-weight layers and the
-LM head carry that to under 1% of the largest logit, while a wiring
-mistake (a wrong position, layer, splice or cache row) moves logits by tens
-of percent.  The argmax must be equal wherever the oracle's top two logits
-are more than twice the bar apart; cells stop at EOS on both sides
+Bars (tiny float32 model; only q, k, v and the caches are bf16 on both
+sides), derived on the CPU in tests/decode_bar.py from the attention bar
+alone -- twice what the reference decoder shows when every attention output
+is moved by 1e-3 on average (independent noise, or one coherent relative
+error per call):
+  * logits of every active cell within LOGIT_REL of the oracle's, relative
+    to max(1, largest logit magnitude);
+  * appended cache rows at layer 0 (a function of the embeddings alone)
+    within one bf16 rounding of the float32-vs-float64 projections; at
+    layers >= 1 each element within ROW_REL of the layer's row rms, and at
+    most a ROW_FLIP_FRAC fraction of the elements with other bits.
+A wiring mistake (a wrong position, layer, splice or cache row) moves logits
+by tens of percent.  The argmax must be equal wherever the oracle's top two
+logits are more than twice the bar apart; cells stop at EOS on both sides
 alike (the EOS id is taken from the first pass, so some cells do stop and
 are skipped from then on)."""
 import numpy as np
 import pytest
 import torch
 
+import decode_bar
 import gpu_common as gc
-import oracle_pins
 import paper_2605_30574_amd as sp
 from oracle import decoder as ref
 from paper_2605_30574_amd import decode
 import workloads
-from workloads.model import ModelConfig, make_weights
+from workloads.model import make_weights
 
 pytestmark = pytest.mark.gpu
 
-LOGIT_REL = 2e-2
+# derived by decode_bar.derive() (test_decode_bar.py checks they still are)
+LOGIT_REL = 0.008
+ROW_REL = 0.033
+ROW_FLIP_FRAC = 0.83
 
 
 @pytest.fixture(scope="module", autouse=True)
@@ -38,19 +46,10 @@ def _gpu():
     sp.load_library()
 
 
-def _f64(wt):
-    f = lambda t: t.double().numpy()
-    return dict(embed=f(wt["embed"]), lm_head=f(wt["lm_head"]), norm_f=f(wt["norm_f"]),
-                layers=[{k: f(v) for k, v in L.items()} for L in wt["layers"]])
-
-
-@pytest.mark.parametrize("name", ["blank-sink", "zero-window5", "diff-G8"])
+@pytest.mark.parametrize("name", decode_bar.CASES)
 def test_decode_loop_matches_oracle(name):
-    t = oracle_pins.tiny
-    w = {"blank-sink": t(dtype="bf16", donor="blank", sink=True),
-         "zero-window5": t(dtype="bf16", donor="zero", window=5),
-         "diff-G8": t(dtype="bf16", donor="diff").with_(n_q_heads=16, n_kv_heads=2)}[name]
-    m = ModelConfig(d_model=96, d_ff=160, vocab=64, eos=5)
+    w = decode_bar.case(name)
+    m = decode_bar.MODEL
     lw = workloads.cell_lw(w)
     C = lw.shape[0]
     wt_cpu = make_weights(w, m, dtype=torch.float32)
@@ -59,7 +58,7 @@ def test_decode_loop_matches_oracle(name):
     caches = [gc.gpu_layer(w, l, n_cells=C) for l in range(w.n_layers)]
     prompts = [{k: v for k, v in gc.host(c).items() if k in ("clean_k", "clean_v", "donor_k", "donor_v")} for c in caches]
     gpu = decode.SweepDecoder(w, m, wt_gpu, caches, lw)
-    cpu = ref.ReferenceDecoder(w, m, _f64(wt_cpu), prompts, lw)
+    cpu = ref.ReferenceDecoder(w, m, decode_bar.f64_weights(wt_cpu), prompts, lw)
     steps = np.zeros(C, dtype=np.int32)
     tokens = np.full(C, 11, dtype=np.int64)   # the token after prefill: the same for every cell
     eos = None   # chosen after the first pass (the token cell 2 emits), so some cells do stop
@@ -91,14 +90,17 @@ def test_decode_loop_matches_oracle(name):
     assert stopped >= 1, f"{name}: no cell reached EOS"
     # the rows the GPU appended are the rows the reference stored: at layer 0
     # (a function of the embeddings alone) to within one bf16 rounding of the
-    # float32-vs-float64 projections, deeper to within the logits' bar
+    # float32-vs-float64 projections, deeper element by element to within the
+    # derived bars
     for l in range(w.n_layers):
         for kind, mine in (("gen_k", cpu.gen_k[l]), ("gen_v", cpu.gen_v[l])):
-            got = ref.from_bf16_bits(workloads.to_numpy(caches[l][kind]))
-            want = ref.from_bf16_bits(mine)
+            got_bits = workloads.to_numpy(caches[l][kind])
             written = mine != 0
             if l == 0:
-                ok = np.allclose(got[written], want[written], rtol=2 ** -7, atol=1e-6)
+                got, want = ref.from_bf16_bits(got_bits), ref.from_bf16_bits(mine)
+                assert np.allclose(got[written], want[written], rtol=2 ** -7, atol=1e-6), f"{name} layer 0: {kind}"
             else:
-                ok = np.abs(got[written] - want[written]).max() <= LOGIT_REL * np.abs(want[written]).max()
-            assert ok, f"{name} layer {l}: {kind}"
+                dev, flip = decode_bar.row_deviation(mine, np.where(written, got_bits, 0).astype(np.uint16))
+                gc.announce(f"decode {name} layer {l} {kind}: deviation {dev:.2e} of rms, {flip:.3f} flipped")
+                assert dev <= ROW_REL, f"{name} layer {l}: {kind} deviation {dev:.2e} of the rows' rms"
+                assert flip <= ROW_FLIP_FRAC, f"{name} layer {l}: {kind} {flip:.3f} of the elements differ"
