@@ -42,7 +42,7 @@ Reported (one JSON line):
               measured after the timed region: time per launch, GB/s of
               the pass's algorithmic bytes, active cells, cell-steps/s.
 
-    python bench.py [--gpus 1] [--steps K] [--warmup W] [--config qwen3-4b]
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--config qwen3-8b] [--also llama3-8b]
 """
 from __future__ import annotations
 
@@ -185,8 +185,27 @@ def spliced_flags(w, layer, step):
 
 # ------------------------------------------------------------------ CPU baseline
 
-def cpu_baseline(w, seconds_cap: float = 30.0):
-    """Time the fp64 oracle (as it stands) on a stratified sample of calls."""
+def host_cpu():
+    """(logical CPUs of this host, CPUs this process may run on, CPU model)."""
+    model = "unknown"
+    try:
+        for ln in open("/proc/cpuinfo"):
+            if ln.startswith("model name"):
+                model = ln.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    try:
+        usable = len(os.sched_getaffinity(0))
+    except AttributeError:
+        usable = os.cpu_count() or 1
+    return os.cpu_count() or 1, usable, model
+
+
+def cpu_baseline(w, seconds_cap: float = 20.0):
+    """Time the fp64 oracle (as it stands) on a stratified sample of calls of
+    workload w: with every thread OpenMP gives it, then with one thread on a
+    smaller sample; plus the full sweep of the tiny workload."""
     import numpy as np
     import oracle
     import workloads
@@ -196,41 +215,69 @@ def cpu_baseline(w, seconds_cap: float = 30.0):
     osh = oracle.shape_of(w)
     lib = oracle.load()
     threads = oracle.max_threads()
+    n_cpu, n_usable, model = host_cpu()
 
-    def one_call(hb, layer, step):
+    def one_call(hb, layer, step, nt):
         q = workloads.to_numpy(workloads.make_q(w, layer, step, device="cpu"))
         t0 = time.perf_counter()
         oracle.attn(osh, layer, step, w.window(layer), w.scale, lw, q, hb["clean_k"], hb["clean_v"],
-                    hb["donor_k"], hb["donor_v"], hb["gen_k"], hb["gen_v"], n_threads=threads, lib=lib)
+                    hb["donor_k"], hb["donor_v"], hb["gen_k"], hb["gen_v"], n_threads=nt, lib=lib)
         return time.perf_counter() - t0
 
-    # pilot (untimed): one call at the middle step sizes the stratified grid
-    # so that the sample takes about seconds_cap; a call's cost is affine in
-    # the step, so the middle step is the grid's average
-    hb = {k: workloads.to_numpy(v) for k, v in workloads.make_layer(w, layers[0], device="cpu").items()}
-    t_mid = max(one_call(hb, layers[0], S // 2), 1e-4)
-    n_s = int(max(4, min(S, seconds_cap / (len(layers) * t_mid))))
-    steps = sorted({min(S - 1, int((i + 0.5) * S / n_s)) for i in range(n_s)})
-    done_bytes, done_time, n_calls = 0, 0.0, 0
-    t_start = time.time()
-    for layer in layers:
-        if layer != layers[0]:
-            hb = {k: workloads.to_numpy(v) for k, v in workloads.make_layer(w, layer, device="cpu").items()}
-        for step in steps:
-            done_time += one_call(hb, layer, step)
-            done_bytes += call_bytes(w, layer, step, spliced_flags(w, layer, step))
-            n_calls += 1
-            if time.time() - t_start > 2 * seconds_cap:   # a bad pilot estimate: stop the sample
+    def sample(nt, cap):
+        # pilot (untimed): one call at the middle step sizes the stratified
+        # grid so that the sample takes about `cap` seconds; a call's cost is
+        # affine in the step, so the middle step is the grid's average
+        hb = {k: workloads.to_numpy(v) for k, v in workloads.make_layer(w, layers[0], device="cpu").items()}
+        t_mid = max(one_call(hb, layers[0], S // 2, nt), 1e-4)
+        n_s = int(max(2, min(S, cap / (len(layers) * t_mid))))
+        steps = sorted({min(S - 1, int((i + 0.5) * S / n_s)) for i in range(n_s)})
+        done_bytes, done_time, n_calls = 0, 0.0, 0
+        t_start = time.time()
+        for layer in layers:
+            if layer != layers[0]:
+                hb = {k: workloads.to_numpy(v) for k, v in workloads.make_layer(w, layer, device="cpu").items()}
+            for step in steps:
+                done_time += one_call(hb, layer, step, nt)
+                done_bytes += call_bytes(w, layer, step, spliced_flags(w, layer, step))
+                n_calls += 1
+                if time.time() - t_start > 2 * cap:   # a bad pilot estimate: stop the sample
+                    break
+            del hb
+            if time.time() - t_start > 2 * cap:
                 break
-        del hb
-        if time.time() - t_start > 2 * seconds_cap:
-            break
-    gbs = done_bytes / done_time / 1e9
-    return {"value": round(gbs, 4), "unit": "GB/s", "cores": threads, "kind": "oracle",
-            "sample": f"{n_calls} calls of {w.name}: layers {layers} x {len(steps)} steps evenly "
-                      f"spaced over [0, {S}) (stratified), "
-                      f"all {w.n_cells} cells x {w.n_q_heads} heads, fp64, {done_time:.1f} s",
-            "calls": n_calls, "seconds": round(done_time, 2)}
+        return done_bytes, done_time, n_calls, len(steps)
+
+    b_all, t_all, n_all, k_all = sample(threads, seconds_cap)
+    b_one, t_one, n_one, k_one = sample(1, seconds_cap / 2)
+    # the tiny f32 workload: its whole sweep (every layer, step and cell), all threads
+    tw = workloads.get(0)
+    tlw, tosh = workloads.cell_lw(tw), oracle.shape_of(tw)
+    t_tiny, tiny_calls = 0.0, 0
+    for layer in range(tw.n_layers):
+        hb = {k: workloads.to_numpy(v) for k, v in workloads.make_layer(tw, layer, device="cpu").items()}
+        for step in range(tw.n_steps):
+            q = workloads.to_numpy(workloads.make_q(tw, layer, step, device="cpu"))
+            t0 = time.perf_counter()
+            oracle.attn(tosh, layer, step, tw.window(layer), tw.scale, tlw, q, hb["clean_k"], hb["clean_v"],
+                        hb["donor_k"], hb["donor_v"], hb["gen_k"], hb["gen_v"], n_threads=threads, lib=lib)
+            t_tiny += time.perf_counter() - t0
+            tiny_calls += 1
+    return {"value": round(b_all / t_all / 1e9, 4), "unit": "GB/s", "cores": threads, "kind": "oracle",
+            "sample": f"{n_all} calls of {w.name}: layers {layers} x {k_all} steps evenly "
+                      f"spaced over [0, {S}) (stratified), all {w.n_cells} cells x {w.n_q_heads} heads, "
+                      f"fp64, {threads} OpenMP threads, {t_all:.1f} s",
+            "calls": n_all, "seconds": round(t_all, 2),
+            # a cell-step is one cell at one step over all N layers: the
+            # stratified sample's calls per second times C / N
+            "cell_steps_per_s": round(n_all / t_all * w.n_cells / N, 3),
+            "host": {"nproc": n_cpu, "usable_cpus": n_usable, "cpu_model": model},
+            "one_thread": {"value": round(b_one / t_one / 1e9, 4), "unit": "GB/s", "calls": n_one,
+                           "seconds": round(t_one, 2),
+                           "sample": f"layers {layers} x {k_one} steps, 1 thread"},
+            "tiny_full_sweep": {"workload": tw.name, "calls": tiny_calls, "cell_steps": tw.n_cells * tw.n_steps,
+                                "seconds": round(t_tiny, 4),
+                                "cell_steps_per_s": round(tw.n_cells * tw.n_steps / t_tiny, 1)}}
 
 
 # ------------------------------------------------------------------ traffic from profiles
@@ -254,6 +301,105 @@ def stored_traffic(w_name: str):
         return None, "malformed counter summary"
 
 
+class _Sweep:
+    pass
+
+
+def timed_sweep(w, K: int, warmup: int, eager: bool, dev, extra_steps=()):
+    """Make workload w's inputs resident, capture one graph per decode step
+    (N launches of splice_decode_attn), replay `warmup` steps, then time K
+    steps evenly spaced over [0, S) between two HIP events on the launch
+    stream.  Returns the buffers, the runner and the timings."""
+    import torch
+
+    import paper_2605_30574_amd as sp
+    import workloads
+    N, S, C = w.n_layers, w.n_steps, w.n_cells
+    r = _Sweep()
+    r.timed_steps = [min(S - 1, int((i + 0.5) * S / K)) for i in range(K)]
+    r.warm_steps = [min(S - 1, int((i + 0.5) * S / max(1, warmup))) for i in range(warmup)]
+    log(f"workload {w.name}: N={N} C={C} Hq={w.n_q_heads} Hkv={w.n_kv_heads} D={w.head_dim} "
+        f"T_p={w.prompt_len} S={S}; timed steps K={K}")
+    t0 = time.time()
+    r.layers = [workloads.make_layer(w, l, device=dev) for l in range(N)]
+    r.qs = [workloads.make_q(w, l, 0, device=dev) for l in range(N)]
+    torch.cuda.synchronize()
+    log(f"inputs resident in HBM ({time.time() - t0:.1f} s, "
+        f"{torch.cuda.memory_allocated() / 2**30:.1f} GiB)")
+    r.shape = sp.make_shape(C, N, w.n_q_heads, w.n_kv_heads, w.head_dim, w.prompt_len, w.span, S,
+                            w.donor == "zero", w.dtype)
+    r.lw = workloads.cell_lw(w)
+    r.ws = sp.new_workspace(r.shape, device=dev)
+    r.out = torch.empty((C, w.n_q_heads, w.head_dim), dtype=torch.float32, device=dev)
+    r.lse = torch.empty((C, w.n_q_heads), dtype=torch.float32, device=dev)
+
+    def issue_step(s: int):
+        for l in range(N):
+            b = r.layers[l]
+            sp.splice_decode_attn(r.shape, sp.make_call(l, s, w.window(l), w.scale), r.lw, r.qs[l],
+                                  b["clean_k"], b["clean_v"], b["donor_k"], b["donor_v"],
+                                  b["gen_k"], b["gen_v"], r.out, r.lse, r.ws)
+
+    r.stream = torch.cuda.Stream(device=dev)
+    r.stream.wait_stream(torch.cuda.current_stream(dev))
+    graphs = {}
+    if not eager:
+        t0 = time.time()
+        for s in sorted(set(r.timed_steps) | set(r.warm_steps) | set(extra_steps)):
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g, stream=r.stream):
+                issue_step(s)
+            graphs[s] = g
+        torch.cuda.synchronize()
+        log(f"captured {len(graphs)} step graphs of {N} launches ({time.time() - t0:.1f} s)")
+    r.graphs = graphs
+
+    def run(steps_list):
+        with torch.cuda.stream(r.stream):
+            for s in steps_list:
+                if eager:
+                    issue_step(s)
+                else:
+                    graphs[s].replay()
+    r.run = run
+
+    run(r.warm_steps)
+    torch.cuda.synchronize()
+    ev0 = torch.cuda.Event(enable_timing=True)
+    ev1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    ev0.record(r.stream)
+    run(r.timed_steps)
+    ev1.record(r.stream)
+    torch.cuda.synchronize()
+    r.ms = ev0.elapsed_time(ev1)
+    r.sec = r.ms / 1e3
+    r.launches = K * N
+    r.alg_bytes = sum(call_bytes(w, l, s, spliced_flags(w, l, s)) for s in r.timed_steps for l in range(N))
+    r.gbs = r.alg_bytes / r.sec / 1e9
+    r.handovers = sp.splice_workspace_handovers(r.ws, r.stream)
+    log(f"timed {r.launches} launches in {r.ms:.2f} ms: {r.gbs:.1f} GB/s algorithmic, "
+        f"{C * K / r.sec:.0f} cell-steps/s, {r.handovers} merges handed over")
+    return r
+
+
+def sweep_summary(w, r, K: int):
+    """The sweep figures of a timed_sweep result, with its roofline."""
+    traffic, traffic_src = stored_traffic(w.name)
+    per_launch = r.alg_bytes / r.launches
+    avg_s = r.sec / r.launches
+    return {"GB/s": round(r.gbs, 2), "pct_of_hbm_peak": round(100 * r.gbs / HBM_PEAK_GBS, 2),
+            "cell_steps_per_s": round(w.n_cells * K / r.sec, 1), "ms_per_step": round(r.ms / K, 4),
+            "steps": K, "merges_handed_over": r.handovers,
+            "roofline": {"bound": "hbm", "achieved": round(per_launch / avg_s / 1e9, 2), "peak": HBM_PEAK_GBS,
+                         "unit": "GB/s", "frac": round(per_launch / avg_s / 1e9 / HBM_PEAK_GBS, 4),
+                         "traffic": traffic, "kernel": launch_kernels(w), "bytes_per_launch": round(per_launch),
+                         "avg_launch_us": round(avg_s * 1e6, 3), "traffic_source": traffic_src},
+            "config": {"workload": w.name, "layers": w.n_layers, "cells": w.n_cells, "q_heads": w.n_q_heads,
+                       "kv_heads": w.n_kv_heads, "head_dim": w.head_dim, "prompt_len": w.prompt_len,
+                       "span": list(w.span), "decode_steps": w.n_steps, "donor": w.donor}}
+
+
 # ------------------------------------------------------------------ main
 
 def main():
@@ -261,7 +407,9 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=0, help="timed decode steps (default: S = one sweep)")
     ap.add_argument("--warmup", type=int, default=8)
-    ap.add_argument("--config", default="qwen3-4b")
+    ap.add_argument("--config", default="qwen3-8b")
+    ap.add_argument("--also", default="llama3-8b",
+                    help="comma-separated workloads whose sweep is timed after the main one ('' for none)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=20.0)
     ap.add_argument("--eager", action="store_true", help="launch without graphs")
@@ -303,69 +451,11 @@ def main():
     w = workloads.get(args.config)
     N, S, C = w.n_layers, w.n_steps, w.n_cells
     K = args.steps if args.steps > 0 else S
-    timed_steps = [min(S - 1, int((i + 0.5) * S / K)) for i in range(K)]
-    warm_steps = [min(S - 1, int((i + 0.5) * S / max(1, args.warmup))) for i in range(args.warmup)]
     bucket_steps = sorted({0, S // 4, S // 2, S - 1})
-
-    log(f"workload {w.name}: N={N} C={C} Hq={w.n_q_heads} Hkv={w.n_kv_heads} D={w.head_dim} "
-        f"T_p={w.prompt_len} S={S}; timed steps K={K}")
-    t0 = time.time()
-    layers = [workloads.make_layer(w, l, device=dev) for l in range(N)]
-    qs = [workloads.make_q(w, l, 0, device=dev) for l in range(N)]
-    torch.cuda.synchronize()
-    log(f"inputs resident in HBM ({time.time() - t0:.1f} s, "
-        f"{torch.cuda.memory_allocated() / 2**30:.1f} GiB)")
-    shape = sp.make_shape(C, N, w.n_q_heads, w.n_kv_heads, w.head_dim, w.prompt_len, w.span, S,
-                          w.donor == "zero", w.dtype)
-    lw = workloads.cell_lw(w)
-    ws = sp.new_workspace(shape, device=dev)
-    out = torch.empty((C, w.n_q_heads, w.head_dim), dtype=torch.float32, device=dev)
-    lse = torch.empty((C, w.n_q_heads), dtype=torch.float32, device=dev)
-
-    def issue_step(s: int):
-        for l in range(N):
-            b = layers[l]
-            sp.splice_decode_attn(shape, sp.make_call(l, s, w.window(l), w.scale), lw, qs[l],
-                                  b["clean_k"], b["clean_v"], b["donor_k"], b["donor_v"],
-                                  b["gen_k"], b["gen_v"], out, lse, ws)
-
-    stream = torch.cuda.Stream(device=dev)
-    stream.wait_stream(torch.cuda.current_stream(dev))
-    graphs = {}
-    if not args.eager:
-        t0 = time.time()
-        for s in sorted(set(timed_steps) | set(warm_steps) | set(bucket_steps)):
-            g = torch.cuda.CUDAGraph()
-            with torch.cuda.graph(g, stream=stream):
-                issue_step(s)
-            graphs[s] = g
-        torch.cuda.synchronize()
-        log(f"captured {len(graphs)} step graphs of {N} launches ({time.time() - t0:.1f} s)")
-
-    def run(steps_list):
-        with torch.cuda.stream(stream):
-            for s in steps_list:
-                if args.eager:
-                    issue_step(s)
-                else:
-                    graphs[s].replay()
-
-    run(warm_steps)
-    torch.cuda.synchronize()
-    ev0 = torch.cuda.Event(enable_timing=True)
-    ev1 = torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    ev0.record(stream)
-    run(timed_steps)
-    ev1.record(stream)
-    torch.cuda.synchronize()
-    ms = ev0.elapsed_time(ev1)
-    sec = ms / 1e3
-    launches = K * N
-    alg_bytes = sum(call_bytes(w, l, s, spliced_flags(w, l, s)) for s in timed_steps for l in range(N))
-    gbs = alg_bytes / sec / 1e9
-    log(f"timed {launches} launches in {ms:.2f} ms: {gbs:.1f} GB/s algorithmic, "
-        f"{C * K / sec:.0f} cell-steps/s")
+    sw = timed_sweep(w, K, args.warmup, args.eager, dev, extra_steps=bucket_steps)
+    layers, qs, shape, lw, ws, out, lse = sw.layers, sw.qs, sw.shape, sw.lw, sw.ws, sw.out, sw.lse
+    stream, run, timed_steps, warm_steps = sw.stream, sw.run, sw.timed_steps, sw.warm_steps
+    ms, sec, launches, alg_bytes, gbs = sw.ms, sw.sec, sw.launches, sw.alg_bytes, sw.gbs
 
     # per-step buckets (outside the timed region): one step's N launches,
     # replayed a few times, at s = 0, S/4, S/2, S - 1
@@ -572,6 +662,22 @@ def main():
                 "avg_launch_us": round(avg_launch_s * 1e6, 3),
                 "traffic_source": traffic_src, "kernel_source_sha256_16": kernel_source_hash()}
 
+    handovers = sw.handovers
+    # the other workloads' sweeps, timed the same way after this one's
+    # buffers are freed
+    del sw, layers, qs, ws, out, lse, run
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    also = {}
+    for name in [n for n in args.also.split(",") if n and n != w.name]:
+        w2 = workloads.get(name)
+        K2 = args.steps if args.steps > 0 else w2.n_steps
+        r2 = timed_sweep(w2, K2, args.warmup, args.eager, dev)
+        also[name] = sweep_summary(w2, r2, K2)
+        del r2
+        torch.cuda.synchronize()
+        torch.cuda.empty_cache()
+
     cpu = None
     if not args.no_cpu_baseline:
         log("timing the fp64 oracle on host cores (CPU baseline)")
@@ -585,6 +691,7 @@ def main():
         "vs_baseline": None, "dtype": w.dtype, "data": "synthetic",
         "pct_of_hbm_peak": round(100 * gbs / HBM_PEAK_GBS, 2),
         "cell_steps_per_s": round(C * K / sec, 1),
+        "merges_handed_over": handovers,
         "config": {"workload": w.name, "layers": N, "cells": C, "q_heads": w.n_q_heads,
                    "kv_heads": w.n_kv_heads, "head_dim": w.head_dim, "prompt_len": w.prompt_len,
                    "span": list(w.span), "decode_steps": S, "donor": w.donor,
@@ -592,6 +699,7 @@ def main():
                    "timed_steps": "evenly spaced over the sweep" if K != S else "full sweep"},
         "roofline": roofline,
         "cpu_baseline": cpu,
+        "also": also,
         "per_step": per_step,
         "per_step_cold": per_step_cold,
         "decode_step": decode_step,

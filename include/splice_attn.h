@@ -58,7 +58,7 @@ extern "C" {
 #define SPLICE_API
 #endif
 
-#define SPLICE_ABI_VERSION 4
+#define SPLICE_ABI_VERSION 5
 #define SPLICE_MAX_CELLS 256
 
 typedef enum {
@@ -94,7 +94,8 @@ typedef struct {
     int32_t layer;         /* l, 0 <= l < N: enters only the splice predicate          */
     int32_t step;          /* s, 0 <= s < gen_capacity: 0-based decode step            */
     int32_t window;        /* sliding window w >= 0 (0: every key visible)            */
-    float scale;           /* softmax scale applied to q.k                            */
+    float scale;           /* softmax scale applied to q.k: finite and > 0, else
+                              SPLICE_EINVAL                                         */
     int32_t split_keys;    /* keys per work item, 0 = library default; else a
                               multiple of 64 in [64, 65536] (tuning and tests)        */
     int32_t merge_wait;    /* bf16 calls with prompt items: how many times a
@@ -144,12 +145,26 @@ SPLICE_API int64_t splice_decode_attn_workspace_bytes(const splice_shape *shape,
 /*
  * Zero a workspace with a fill kernel enqueued on `stream` (no memset node,
  * so it may be graph-captured).  Required once before a workspace's first
- * splice_decode_attn / splice_decode_step: the workspace starts with the
+ * splice_decode_attn / splice_decode_step: the workspace starts with a
+ * 256-byte statistics block (splice_workspace_handovers) and the
  * per-(cell, KV head) arrival counters, which must start at zero; every call
  * re-arms the counters it used, so later calls need no re-initialisation.
  * workspace must be 256-byte aligned and workspace_bytes a multiple of 4.
  */
 SPLICE_API int32_t splice_workspace_init(void *workspace, size_t workspace_bytes, void *stream);
+
+/*
+ * Merges handed over since splice_workspace_init: the number of (cell, KV
+ * head) pairs of bf16 calls whose generated-row item stopped waiting for the
+ * prompt partials (merge_wait ran out, or merge_wait < 0) and left the merge
+ * to the last item to finish.  The result does not depend on it (both merge
+ * sites fold in one order); it counts how often the slower route ran, which
+ * should be 0 with the default bound.  Reads 4 bytes of the workspace's
+ * statistics block back to the host on `stream` and waits for the stream.
+ * Negative splice_status on a NULL or misaligned workspace, one smaller than
+ * 256 bytes, or a failed copy.
+ */
+SPLICE_API int64_t splice_workspace_handovers(const void *workspace, size_t workspace_bytes, void *stream);
 
 /*
  * Spliced single-query GQA decode attention for C sweep cells at one

@@ -13,7 +13,8 @@ from .splice import (EXPORTS, LIB_PATH, SPLICE_BF16, SPLICE_DONOR_BUFFER, SPLICE
                      SpliceShape, load_library, make_call, make_shape, new_workspace,
                      splice_abi_version, splice_decode_attn, splice_decode_attn_workspace_bytes,
                      splice_decode_forked, splice_decode_step,
-                     splice_kv_build, splice_status_str, splice_visible_len, splice_workspace_init,
+                     splice_kv_build, splice_status_str, splice_visible_len, splice_workspace_handovers,
+                     splice_workspace_init,
                      status_name)
 
 __all__ = [n for n in dir() if not n.startswith("_")]

@@ -17,6 +17,7 @@ struct AttnArgs {
     const char *ck, *cv, *dk, *dv, *gk, *gv;
     float *out, *lse, *part;
     int *counters;
+    int *stats;            // workspace statistics: [0] merges handed over (see fused_gen_item)
     uint32_t part_bytes;   // size of the partial-result region (< 2^31)
     int C, Hq, Hkv, Tp, cap;
     int jp0, i0, n_gen, sa, sb;
@@ -907,15 +908,20 @@ __device__ int fused_gen_item(const AttnArgs &a, int item, char *lds, int *s_lis
         const bool mine = lane < n_pairs && a.n_p > 0 && cell_active(a, c0 + lane);
         const int *cnt = a.counters + (c0 + (mine ? lane : 0)) * a.Hkv + g;
         bool done = !mine;
-        int polls = 0;   // the same in every lane
-        while (true) {
+        // wait_polls == 0: never look, so every pair of the item is handed
+        // over (the counter is not read even when the partials are in)
+        for (int polls = 0; polls < a.wait_polls; ++polls) {   // polls: the same in every lane
             if (!done) done = __hip_atomic_load(cnt, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) >= a.n_p;
-            if (__all(done) || polls >= a.wait_polls) break;
+            if (__all(done)) break;
             __builtin_amdgcn_s_sleep(4);
-            ++polls;
         }
         const bool ready = __all(done);
         if (lane == 0) s_list[0] = ready ? -1 : 0;
+        // count the pairs this item hands over (the ones that have prompt
+        // partials to wait for); a fallback the caller can read back
+        const uint64_t handed = __ballot(mine);
+        if (!ready && lane == 0 && handed)
+            __hip_atomic_fetch_add(a.stats, (int)__popcll(handed), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
     __syncthreads();   // also: every wave is done with its V^T tile
     const bool ready = s_list[0] < 0;

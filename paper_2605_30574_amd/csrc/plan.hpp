@@ -75,7 +75,9 @@ inline int32_t validate_call(const splice_shape &sh, const splice_call *call) {
     if (call->layer < 0 || call->layer >= sh.n_layers) return SPLICE_ESHAPE;
     if (call->step < 0 || call->step >= sh.gen_capacity) return SPLICE_ESHAPE;
     if (call->window < 0) return SPLICE_ESHAPE;
-    if (!isfinite(call->scale)) return SPLICE_EINVAL;
+    // the bf16 kernels mask raw q.k with -inf and scale afterwards, which
+    // needs a positive scale; a softmax scale is positive in every model
+    if (!isfinite(call->scale) || !(call->scale > 0.f)) return SPLICE_EINVAL;
     if (call->split_keys != 0 &&
         (call->split_keys < 64 || call->split_keys > 65536 || call->split_keys % 64 != 0))
         return SPLICE_EINVAL;
@@ -323,18 +325,26 @@ inline AttnPlan plan_attn(const splice_shape &sh, const splice_call &call, int n
 }
 
 struct WorkspaceLayout {
+    size_t stats_off;   // kStatsBytes of statistics (the hand-over count), kept across calls
     size_t counters_off, counters_bytes;
     size_t part_off, part_bytes;
     size_t total;
 };
 
-// Counters [C][Hkv] (int32), then one partial slot per (cell, KV head, chunk).
+// Statistics words at the start of a workspace (int32): [0] the number of
+// (cell, KV head) merges handed over by a generated-row item whose bounded
+// wait ran out, counted since splice_workspace_init.
+constexpr size_t kStatsBytes = 256;
+
+// Statistics, counters [C][Hkv] (int32), then one partial slot per (cell,
+// KV head, chunk).
 inline WorkspaceLayout workspace_layout(const splice_shape &sh, int n_slots) {
     WorkspaceLayout w;
     const int64_t pairs = (int64_t)sh.n_cells * sh.n_kv_heads;
-    w.counters_off = 0;
+    w.stats_off = 0;
+    w.counters_off = kStatsBytes;
     w.counters_bytes = (size_t)round_up(pairs * 4, 256);
-    w.part_off = w.counters_bytes;
+    w.part_off = w.counters_off + w.counters_bytes;
     w.part_bytes = (size_t)pairs * (size_t)n_slots * (size_t)slot_floats(group_of(sh), sh.head_dim) * 4;
     w.total = w.part_off + w.part_bytes;
     if (w.total < 256) w.total = 256;

@@ -227,6 +227,16 @@ int32_t splice_workspace_init(void *workspace, size_t workspace_bytes, void *str
     return launch_status();
 }
 
+int64_t splice_workspace_handovers(const void *workspace, size_t workspace_bytes, void *stream) {
+    if (!workspace || !splice::aligned(workspace, 256)) return SPLICE_EINVAL;
+    if (workspace_bytes < splice::kStatsBytes) return SPLICE_EWORKSPACE;
+    int32_t count = 0;
+    if (hipMemcpyAsync(&count, workspace, sizeof(count), hipMemcpyDeviceToHost, (hipStream_t)stream) != hipSuccess)
+        return SPLICE_EHIP;
+    if (hipStreamSynchronize((hipStream_t)stream) != hipSuccess) return SPLICE_EHIP;
+    return count;
+}
+
 }  // extern "C"
 
 namespace {
@@ -331,6 +341,7 @@ int32_t decode_attn_impl(const splice_shape *shape, const splice_call *call, con
     a.kn = (const char *)k_new; a.vn = (const char *)v_new;
     a.out = out; a.lse = lse;
     a.counters = (int *)((char *)workspace + wl.counters_off);
+    a.stats = (int *)((char *)workspace + wl.stats_off);
     a.part = (float *)((char *)workspace + wl.part_off);
     if (wl.part_bytes >= ((size_t)1 << 31)) return SPLICE_EUNSUPPORTED;
     a.part_bytes = (uint32_t)(wl.part_bytes > 0 ? wl.part_bytes : 16);

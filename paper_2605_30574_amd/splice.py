@@ -24,11 +24,11 @@ SPLICE_DONOR_BUFFER, SPLICE_DONOR_ZERO = 0, 1
 SPLICE_BF16, SPLICE_F32 = 0, 1
 SPLICE_SRC_CLEAN, SPLICE_SRC_DONOR, SPLICE_SRC_ZERO, SPLICE_SRC_GEN = 0, 1, 2, 3
 SPLICE_MAX_CELLS = 256
-SPLICE_ABI_VERSION = 4   # layout of SpliceShape / SpliceCall below
+SPLICE_ABI_VERSION = 5   # layout of SpliceShape / SpliceCall below
 
 EXPORTS = ("splice_abi_version", "splice_status_str", "splice_visible_len", "splice_kv_build",
            "splice_decode_attn_workspace_bytes", "splice_workspace_init", "splice_decode_attn",
-           "splice_decode_step", "splice_decode_forked")
+           "splice_decode_step", "splice_decode_forked", "splice_workspace_handovers")
 
 
 class SpliceShape(ctypes.Structure):
@@ -75,6 +75,8 @@ def load_library(path: str = LIB_PATH):
     lib.splice_decode_attn_workspace_bytes.argtypes = [shp, cal]
     lib.splice_workspace_init.restype = i32
     lib.splice_workspace_init.argtypes = [vp, ctypes.c_size_t, vp]
+    lib.splice_workspace_handovers.restype = ctypes.c_int64
+    lib.splice_workspace_handovers.argtypes = [vp, ctypes.c_size_t, vp]
     lib.splice_decode_attn.restype = i32
     lib.splice_decode_attn.argtypes = [shp, cal, i32p, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp,
                                        ctypes.c_size_t, vp]
@@ -198,6 +200,14 @@ def splice_workspace_init(workspace, stream=None) -> None:
     p, dev = _dev_ptr(workspace, "workspace", None, None)
     nbytes = workspace.numel() * workspace.element_size()
     _check(load_library().splice_workspace_init(p, nbytes, _stream_ptr(stream, dev)), "splice_workspace_init")
+
+
+def splice_workspace_handovers(workspace, stream=None) -> int:
+    """Merges handed over since the workspace was initialised (synchronises ``stream``)."""
+    p, dev = _dev_ptr(workspace, "workspace", None, None)
+    nbytes = workspace.numel() * workspace.element_size()
+    return _check(load_library().splice_workspace_handovers(p, nbytes, _stream_ptr(stream, dev)),
+                  "splice_workspace_handovers")
 
 
 def new_workspace(shape: SpliceShape, call: Optional[SpliceCall] = None, device="cuda", stream=None):

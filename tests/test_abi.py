@@ -25,7 +25,7 @@ def test_library_exports_every_declared_symbol():
     lib = sp.load_library()
     for name in declared:
         assert hasattr(lib, name), name
-    assert sp.splice_abi_version() == 4
+    assert sp.splice_abi_version() == 5
 
 
 def test_single_hip_runtime_mapped():
@@ -85,6 +85,9 @@ def test_bad_enums():
     (sp.make_call(0, -1, 0, 1.0), sp.SPLICE_ESHAPE),
     (sp.make_call(0, 0, -3, 1.0), sp.SPLICE_ESHAPE),       # negative window
     (sp.make_call(0, 0, 0, float("nan")), sp.SPLICE_EINVAL),
+    (sp.make_call(0, 0, 0, float("inf")), sp.SPLICE_EINVAL),
+    (sp.make_call(0, 0, 0, 0.0), sp.SPLICE_EINVAL),         # the bf16 kernels need scale > 0
+    (sp.make_call(0, 0, 0, -0.125), sp.SPLICE_EINVAL),
     (sp.make_call(0, 0, 0, 1.0, split_keys=100), sp.SPLICE_EINVAL),
     (sp.make_call(0, 0, 0, 1.0, split_keys=32), sp.SPLICE_EINVAL),
 ])

@@ -72,8 +72,9 @@ def test_merge_site_does_not_change_bits(donor):
     """A generated-row item merges its (cell, KV head) in place after waiting
     for the prompt partials, or -- past its polling bound -- leaves the merge
     to the last item to finish.  Both follow one fold order, so the bits are
-    the same whichever item merged; merge_wait < 0 forces the hand-over on
-    every pair and 1 mixes the two within a call."""
+    the same whichever item merged.  merge_wait < 0 never polls, so every
+    pair takes the hand-over route (the workspace counts C * Hkv hand-overs);
+    the default bound takes none; 1 poll mixes the two within a call."""
     w = _w().with_(donor=donor)
     lw = workloads.cell_lw(w)
     layer, step = 1, 150
@@ -81,13 +82,23 @@ def test_merge_site_does_not_change_bits(donor):
     hb = gc.host(bufs)
     q = workloads.make_q(w, layer, step, device="cuda")
     ref_o, ref_l = gc.run_oracle(w, layer, step, hb, workloads.to_numpy(q), lw)
+    shape = gc.shape_of(w)
+    pairs = w.n_cells * w.n_kv_heads
     gc.announce(f"merge site donor={donor}: in place")
-    o_w, l_w = gc.run_attn(w, layer, step, bufs, q, lw, split=64)
+    ws = sp.new_workspace(shape, sp.make_call(layer, step, 0, w.scale, 64))
+    o_w, l_w = gc.run_attn(w, layer, step, bufs, q, lw, split=64, ws=ws)
     gc.assert_attn_close(o_w, l_w, ref_o, ref_l, "in place")
+    assert sp.splice_workspace_handovers(ws) == 0, "the default bound handed a merge over"
     for mw in (-1, 1):
         gc.announce(f"merge site donor={donor}: merge_wait={mw}")
-        o_h, l_h = gc.run_attn(w, layer, step, bufs, q, lw, split=64, merge_wait=mw)
+        ws = sp.new_workspace(shape, sp.make_call(layer, step, 0, w.scale, 64))
+        o_h, l_h = gc.run_attn(w, layer, step, bufs, q, lw, split=64, merge_wait=mw, ws=ws)
         assert np.array_equal(o_h, o_w) and np.array_equal(l_h, l_w), f"merge_wait={mw}"
+        n = sp.splice_workspace_handovers(ws)
+        if mw < 0:
+            assert n == pairs, f"merge_wait=-1 handed over {n} of {pairs} merges"
+        else:
+            assert 0 <= n <= pairs
 
 
 def test_split_changes_only_rounding():
@@ -108,7 +119,7 @@ def test_split_changes_only_rounding():
         gc.assert_attn_close(o, l, results[0][0], results[0][1], "split vs split")
 
 
-def test_workspace_reuse_across_calls():
+def test_workspace_reuse_across_steps_and_splits():
     """One workspace serves a sequence of calls of different sizes; each
     call writes every partial slot it reads, so stale contents never leak."""
     w = _w()
@@ -171,15 +182,13 @@ def test_graph_replay_matches_eager():
         torch.cuda.synchronize()
 
 
-def test_workspace_reused_across_calls():
-    """One workspace serves a sequence of calls that alternate between the two
-    merge protocols (at most 8 prompt chunks: the generated-row item polls
-    the prompt slots in a bank per (cell, KV head); more: counters and a flat
-    region), change the slot count, hand the merge over (merge_wait < 0) or
-    mix both sites (1), and skip finished cells (a ragged decode step).  Every
-    call must give the bits the same call gives on a fresh workspace: what a
-    call leaves behind (slot data, bank states, counters) never reaches the
-    next one."""
+def test_workspace_reuse_gives_fresh_workspace_bits():
+    """One workspace serves a sequence of calls that change the slot count
+    (the split), hand every merge over (merge_wait < 0) or mix both merge
+    sites (1), and skip finished cells (a ragged decode step).  Every call
+    must give the bits the same call gives on a fresh workspace: what a call
+    leaves behind (partial slots, arrival counters) never reaches the next
+    one."""
     w = _w().with_(prompt_len=1100, span=(40, 1060))
     lw = workloads.cell_lw(w)
     C = lw.shape[0]
