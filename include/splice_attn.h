@@ -58,7 +58,7 @@ extern "C" {
 #define SPLICE_API
 #endif
 
-#define SPLICE_ABI_VERSION 5
+#define SPLICE_ABI_VERSION 6
 #define SPLICE_MAX_CELLS 256
 
 typedef enum {
@@ -186,6 +186,32 @@ SPLICE_API int32_t splice_decode_attn(const splice_shape *shape, const splice_ca
                            const void *gen_k, const void *gen_v,
                            float *out, float *lse,
                            void *workspace, size_t workspace_bytes,
+                           void *stream);
+
+/*
+ * splice_decode_attn without a workspace argument and without allocating:
+ * for callers that cannot call hipMalloc (code under HIP graph capture,
+ * serving loops that must not allocate, harnesses that forbid it).  The
+ * split-K partials and arrival counters live in a library-owned device
+ * array of SPLICE_NOALLOC_WORKSPACE_BYTES bytes, one per GPU, held until
+ * the process ends; calls whose splice_decode_attn_workspace_bytes(shape,
+ * call) exceeds it return SPLICE_EWORKSPACE before any device work.  The
+ * first call on a device takes the array's address and clears it with a
+ * fill kernel on `stream` (make that first call outside graph capture);
+ * every later call finds the arrival counters at zero, because each call
+ * re-arms the counters it uses.  All calls on one GPU share the array:
+ * calls that overlap on one GPU (other streams, other threads) race and must
+ * be ordered by the caller, e.g. on one stream.  Arguments, results, errors
+ * and bits are those of splice_decode_attn (same kernels, same plan).
+ */
+#define SPLICE_NOALLOC_WORKSPACE_BYTES ((size_t)32 << 20)
+SPLICE_API int32_t splice_decode_attn_noalloc(const splice_shape *shape, const splice_call *call,
+                           const int32_t *cell_LW,
+                           const void *q,
+                           const void *clean_k, const void *clean_v,
+                           const void *donor_k, const void *donor_v,
+                           const void *gen_k, const void *gen_v,
+                           float *out, float *lse,
                            void *stream);
 
 /*

@@ -11,7 +11,8 @@ from .splice import (EXPORTS, LIB_PATH, SPLICE_BF16, SPLICE_DONOR_BUFFER, SPLICE
                      SPLICE_EWORKSPACE, SPLICE_F32, SPLICE_MAX_CELLS, SPLICE_OK, SPLICE_SRC_CLEAN,
                      SPLICE_SRC_DONOR, SPLICE_SRC_GEN, SPLICE_SRC_ZERO, SpliceCall, SpliceError,
                      SpliceShape, load_library, make_call, make_shape, new_workspace,
-                     splice_abi_version, splice_decode_attn, splice_decode_attn_workspace_bytes,
+                     splice_abi_version, splice_decode_attn, splice_decode_attn_noalloc,
+                     splice_decode_attn_workspace_bytes,
                      splice_decode_forked, splice_decode_step,
                      splice_kv_build, splice_status_str, splice_visible_len, splice_workspace_handovers,
                      splice_workspace_init,

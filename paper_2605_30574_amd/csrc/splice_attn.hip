@@ -42,6 +42,8 @@
 #include <stdint.h>
 #include <string.h>
 
+#include <mutex>
+
 #include "attn_kernels.hpp"
 #include "plan.hpp"
 #include "splice_attn.h"
@@ -409,6 +411,59 @@ int32_t splice_decode_attn(const splice_shape *shape, const splice_call *call, c
                            size_t workspace_bytes, void *stream) {
     return decode_attn_impl(shape, call, cell_LW, nullptr, -1, q, nullptr, nullptr, clean_k, clean_v, donor_k,
                             donor_v, gen_k, gen_v, out, lse, workspace, workspace_bytes, stream);
+}
+
+}  // extern "C"
+
+namespace {
+
+// The allocation-free entry point's workspace: one array per GPU, held until
+// the process ends.  In host code `scratch` is only a stand-in for the
+// symbol; its device address comes from hipGetSymbolAddress, once per device.
+static __device__ __align__(256) char scratch[SPLICE_NOALLOC_WORKSPACE_BYTES];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void *g_scratch[kMaxDevices];   // device address of `scratch` on each device, set once
+
+// The current device's scratch array.  The first call on a device takes its
+// address and clears it with the fill kernel on `stream` (the arrival
+// counters must start at zero; every call re-arms the counters it used, so
+// the array is left zeroed for the next call).
+int32_t device_scratch(void *stream, void **ptr) {
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return SPLICE_EHIP;
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch[dev]) {
+        void *p = nullptr;
+        if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return SPLICE_EHIP;
+        const size_t words = SPLICE_NOALLOC_WORKSPACE_BYTES / 4;
+        hipLaunchKernelGGL(fill_kernel, dim3(4096), dim3(kThreads), 0, (hipStream_t)stream, (uint32_t *)p, words);
+        if (hipGetLastError() != hipSuccess) return SPLICE_EHIP;
+        g_scratch[dev] = p;
+    }
+    *ptr = g_scratch[dev];
+    return SPLICE_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int32_t splice_decode_attn_noalloc(const splice_shape *shape, const splice_call *call, const int32_t *cell_LW,
+                                   const void *q, const void *clean_k, const void *clean_v, const void *donor_k,
+                                   const void *donor_v, const void *gen_k, const void *gen_v, float *out, float *lse,
+                                   void *stream) {
+    // validation and the size check come first: a call that does not fit is
+    // rejected before any device work
+    const int64_t need = splice_decode_attn_workspace_bytes(shape, call);
+    if (need < 0) return (int32_t)need;
+    if (need > (int64_t)SPLICE_NOALLOC_WORKSPACE_BYTES) return SPLICE_EWORKSPACE;
+    void *ws = nullptr;
+    const int32_t rc = device_scratch(stream, &ws);
+    if (rc != SPLICE_OK) return rc;
+    return decode_attn_impl(shape, call, cell_LW, nullptr, -1, q, nullptr, nullptr, clean_k, clean_v, donor_k,
+                            donor_v, gen_k, gen_v, out, lse, ws, SPLICE_NOALLOC_WORKSPACE_BYTES, stream);
 }
 
 int32_t splice_decode_step(const splice_shape *shape, const splice_call *call, const int32_t *cell_LW,

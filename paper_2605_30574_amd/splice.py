@@ -24,11 +24,13 @@ SPLICE_DONOR_BUFFER, SPLICE_DONOR_ZERO = 0, 1
 SPLICE_BF16, SPLICE_F32 = 0, 1
 SPLICE_SRC_CLEAN, SPLICE_SRC_DONOR, SPLICE_SRC_ZERO, SPLICE_SRC_GEN = 0, 1, 2, 3
 SPLICE_MAX_CELLS = 256
-SPLICE_ABI_VERSION = 5   # layout of SpliceShape / SpliceCall below
+SPLICE_ABI_VERSION = 6   # layout of SpliceShape / SpliceCall below
 
 EXPORTS = ("splice_abi_version", "splice_status_str", "splice_visible_len", "splice_kv_build",
            "splice_decode_attn_workspace_bytes", "splice_workspace_init", "splice_decode_attn",
-           "splice_decode_step", "splice_decode_forked", "splice_workspace_handovers")
+           "splice_decode_step", "splice_decode_forked", "splice_workspace_handovers",
+           "splice_decode_attn_noalloc")
+SPLICE_NOALLOC_WORKSPACE_BYTES = 32 << 20
 
 
 class SpliceShape(ctypes.Structure):
@@ -80,6 +82,8 @@ def load_library(path: str = LIB_PATH):
     lib.splice_decode_attn.restype = i32
     lib.splice_decode_attn.argtypes = [shp, cal, i32p, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp,
                                        ctypes.c_size_t, vp]
+    lib.splice_decode_attn_noalloc.restype = i32
+    lib.splice_decode_attn_noalloc.argtypes = [shp, cal, i32p, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp]
     lib.splice_decode_step.restype = i32
     lib.splice_decode_step.argtypes = [shp, cal, i32p, i32p, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp,
                                        vp, ctypes.c_size_t, vp]
@@ -260,6 +264,28 @@ def splice_decode_attn(shape: SpliceShape, call: SpliceCall, cell_LW, q, clean_k
     lw, lwp = _cells(cell_LW, C)
     _check(lib.splice_decode_attn(ctypes.byref(shape), ctypes.byref(call), lwp, qp, ck, cv, dk, dv, gk, gv,
                                   op, lp, wp, wbytes, _stream_ptr(stream, dev)), "splice_decode_attn")
+
+
+def splice_decode_attn_noalloc(shape: SpliceShape, call: SpliceCall, cell_LW, q, clean_k, clean_v, donor_k,
+                               donor_v, gen_k, gen_v, out, lse, stream=None) -> None:
+    """splice_decode_attn with the library's own per-GPU workspace array
+    (no workspace argument, nothing allocated)."""
+    import torch
+    lib = load_library()
+    C, Hq, Hkv, D = shape.n_cells, shape.n_q_heads, shape.n_kv_heads, shape.head_dim
+    dt = _torch_dtype(shape)
+    n_prompt = Hkv * shape.prompt_len * D
+    qp, dev = _dev_ptr(q, "q", C * Hq * D, dt)
+    ck, _ = _dev_ptr(clean_k, "clean_k", n_prompt, dt, dev)
+    cv, _ = _dev_ptr(clean_v, "clean_v", n_prompt, dt, dev)
+    dk, dv = _donors(shape, donor_k, donor_v, dt, n_prompt, dev)
+    gk, _ = _dev_ptr(gen_k, "gen_k", C * Hkv * shape.gen_capacity * D, dt, dev)
+    gv, _ = _dev_ptr(gen_v, "gen_v", C * Hkv * shape.gen_capacity * D, dt, dev)
+    op, _ = _dev_ptr(out, "out", C * Hq * D, torch.float32, dev)
+    lp, _ = _dev_ptr(lse, "lse", C * Hq, torch.float32, dev)
+    lw, lwp = _cells(cell_LW, C)
+    _check(lib.splice_decode_attn_noalloc(ctypes.byref(shape), ctypes.byref(call), lwp, qp, ck, cv, dk, dv, gk, gv,
+                                          op, lp, _stream_ptr(stream, dev)), "splice_decode_attn_noalloc")
 
 
 def _steps(cell_step, n_cells: int):

@@ -25,7 +25,7 @@ def test_library_exports_every_declared_symbol():
     lib = sp.load_library()
     for name in declared:
         assert hasattr(lib, name), name
-    assert sp.splice_abi_version() == 5
+    assert sp.splice_abi_version() == 6
 
 
 def test_single_hip_runtime_mapped():
@@ -202,3 +202,21 @@ def test_decode_forked_validation_before_device_access():
     assert forked(sh, cells, 1) == sp.SPLICE_ESHAPE            # the trunk would be spliced
     assert forked(sh, cells, 0, wbytes=16) == sp.SPLICE_EWORKSPACE
     assert forked(_shape(dtype="f32"), cells, 0) == sp.SPLICE_EUNSUPPORTED
+
+
+def test_noalloc_rejects_calls_beyond_its_array_before_device_access():
+    """A call whose workspace would exceed the library's per-GPU array is
+    refused on the host (no GPU is touched here)."""
+    lib = sp.load_library()
+    sh = _shape(n_cells=256, n_q_heads=32, n_kv_heads=8, head_dim=128, prompt_len=8192, span=(128, 8128),
+                gen_capacity=1024, donor_zero=False, dtype="bf16")
+    call = sp.make_call(0, 0, 0, 128 ** -0.5, split_keys=512)   # 16 prompt chunks: 17 slots per pair
+    assert sp.splice_decode_attn_workspace_bytes(sh, call) > S.SPLICE_NOALLOC_WORKSPACE_BYTES
+    lw = (ctypes.c_int32 * 512)(*([0, 0] * 256))
+    fake = ctypes.c_void_p(0x1000)   # never dereferenced
+    assert lib.splice_decode_attn_noalloc(ctypes.byref(sh), ctypes.byref(call), lw, *([fake] * 9), None) == \
+        sp.SPLICE_EWORKSPACE
+    # a bad argument is reported as such before the size is looked at
+    bad = sp.make_call(0, 0, 0, float("nan"))
+    assert lib.splice_decode_attn_noalloc(ctypes.byref(sh), ctypes.byref(bad), lw, *([fake] * 9), None) == \
+        sp.SPLICE_EINVAL
