@@ -7,7 +7,7 @@
  * T_p slots per layer.  For every layer l >= L, from decode step W on, the
  * prompt-span slots are read from a donor cache of the same length (or are
  * all-zero for the ZERO donor) instead of the clean cache; generated entries
- * are never modified.  Readings fixed by this ABI:
+ * keep their values.  Readings fixed by this ABI:
  *   - step s is 0-based (s = 0 is the first decode pass after prefill) and
  *     cell c is spliced at (layer, s) iff layer >= L_c and s >= W_c;
  *   - only slots [span_lo, span_hi) are replaced ([0, T_p) is the

@@ -13,7 +13,8 @@
  *     onset W: decode steps before W use the unmodified cache; from step W on
  *     the prompt-span entries of every patched layer hold the donor's entries
  *     and keep holding them to the end (in-place, permanent replacement).
- *     Generated-span entries are never modified.
+ *     The rows the decode itself generates stay as written: a splice touches
+ *     only prompt slots.
  *   Donors (Table 1): ZERO = all-zero K and V; the other forms are buffers of
  *     the same prompt length, aligned slot for slot with the target prompt.
  *
