@@ -41,6 +41,11 @@ struct AttnArgs {
     float qk_scale;   // scale * log2(e)
     uint32_t spliced[SPLICE_MAX_CELLS / 32];
     uint8_t order[SPLICE_MAX_CELLS];   // clean cells, then spliced cells
+    // bf16 generated-row items: the cells that have generated rows to stream
+    // (active, and under a forked sweep diverged), longest first; item i
+    // serves gorder[i * gen_pairs ..]
+    int n_gen_cells;
+    uint8_t gorder[SPLICE_MAX_CELLS];
 };
 
 
@@ -782,7 +787,7 @@ __device__ __forceinline__ void gen_merge_in_place(const AttnArgs &a, const Wave
             pe[u] = e / UPG;
             he[u] = (e % UPG) / (D / 4);
             de[u] = 4 * (e % (D / 4));
-            const uint32_t sbase = slot_off(a, c0 + pe[u], g, 0);
+            const uint32_t sbase = slot_off(a, a.gorder[c0 + pe[u]], g, 0);
             const uint32_t o_off = (uint32_t)(he[u] * D + de[u]) * 4u;
             const uint32_t m_off = (uint32_t)(G * D + he[u]) * 4u, l_off = (uint32_t)(G * D + G + he[u]) * 4u;
 #pragma unroll
@@ -798,8 +803,8 @@ __device__ __forceinline__ void gen_merge_in_place(const AttnArgs &a, const Wave
         __syncthreads();   // the staged partials are visible (first round); no-op ordering after
         static_for<0, U>([&](auto u) {
             const int e = e0 + (int)u * NT + tid;
-            const int cq = c0 + pe[u];
-            if (e < total && cell_active(a, cq)) {
+            const int cq = a.gorder[c0 + pe[u]];
+            if (e < total) {
                 const int h = he[u], d = de[u], w0 = pe[u] * wpp;
                 // this item's partial: its waves combined
                 float Mg = -INFINITY;
@@ -836,9 +841,11 @@ __device__ __forceinline__ void gen_merge_in_place(const AttnArgs &a, const Wave
     }
 }
 
-// Generated-row item: KV head g and P = a.gen_pairs consecutive cells, wpp =
-// NW / P waves per (cell, KV head) pair streaming that cell's generated rows
-// (interleaved tiles).  After streaming, the first wave polls the pairs' counters (a lane per pair)
+// Generated-row item: KV head g and P = a.gen_pairs consecutive cells of
+// a.gorder (the cells with generated rows to stream, longest first, so the
+// grid holds no empty items and the longest streams are dispatched first),
+// wpp = NW / P waves per (cell, KV head) pair streaming that cell's generated
+// rows (interleaved tiles).  After streaming, the first wave polls the pairs' counters (a lane per pair)
 // until every prompt chunk has stored its partial (at most a.wait_polls polls
 // in all; prompt items have lower block indices and never wait, so they are
 // dispatched first and finish).  Then this item merges in place: its own
@@ -853,17 +860,16 @@ __device__ int fused_gen_item(const AttnArgs &a, int item, char *lds, int *s_lis
     constexpr int NW = Fused<D>::NW, NT = Fused<D>::NT;
     const int P = a.gen_pairs, wpp = NW / P;
     const int g = item % a.Hkv;
-    const int c0 = (item / a.Hkv) * P;
-    const int n_pairs = min(P, a.C - c0);
+    const int c0 = (item / a.Hkv) * P;   // first of the item's cells in gorder
+    const int n_pairs = min(P, a.n_gen_cells - c0);
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-    const int c = c0 + wave / wpp;   // this wave's cell
-    const bool valid = c < a.C && cell_active(a, c);
+    const bool valid = wave / wpp < n_pairs;
+    const int c = valid ? a.gorder[c0 + wave / wpp] : 0;   // this wave's cell
     const int col = threadIdx.x & 15;
     if (a.kn) {   // append: row s of each active cell's generated K and V
         constexpr int U = W::ROW / 16;   // 16-byte units of a row
         for (int t = threadIdx.x; t < n_pairs * 2 * U; t += NT) {
-            const int cq = c0 + t / (2 * U), kv = (t / U) & 1, u = t % U;
-            if (!cell_active(a, cq)) continue;
+            const int cq = a.gorder[c0 + t / (2 * U)], kv = (t / U) & 1, u = t % U;
             const size_t src = ((size_t)cq * a.Hkv + g) * W::ROW + 16 * u;
             const size_t dst = (((size_t)cq * a.Hkv + g) * (size_t)a.cap + cell_geo(a, cq).s) * W::ROW + 16 * u;
             char *to = const_cast<char *>(kv ? a.gv : a.gk);
@@ -905,8 +911,8 @@ __device__ int fused_gen_item(const AttnArgs &a, int item, char *lds, int *s_lis
 
     if (threadIdx.x < 64) {   // wave 0: lane q polls the counter of pair q, all pairs at once
         const int lane = threadIdx.x;
-        const bool mine = lane < n_pairs && a.n_p > 0 && cell_active(a, c0 + lane);
-        const int *cnt = a.counters + (c0 + (mine ? lane : 0)) * a.Hkv + g;
+        const bool mine = lane < n_pairs && a.n_p > 0;
+        const int *cnt = a.counters + (int)a.gorder[c0 + (mine ? lane : 0)] * a.Hkv + g;
         bool done = !mine;
         // wait_polls == 0: never look, so every pair of the item is handed
         // over (the counter is not read even when the partials are in)
@@ -934,8 +940,7 @@ __device__ int fused_gen_item(const AttnArgs &a, int item, char *lds, int *s_lis
             gen_merge_in_place<D, G, NW, 16, 1>(a, S, lds, wpp, n_pairs, c0, g);
         } else {
         waves_merge<D, G, NW>(S, lds, wpp, n_pairs, [&](int q, int h, int d, float Mg, float Lg, f32x4_t Og) {
-            const int cq = c0 + q;
-            if (!cell_active(a, cq)) return;
+            const int cq = a.gorder[c0 + q];
             const uint32_t sbase = slot_off(a, cq, g, 0);
             const uint32_t o_off = (uint32_t)(h * D + d) * 4u;
             const uint32_t m_off = (uint32_t)(G * D + h) * 4u, l_off = (uint32_t)(G * D + G + h) * 4u;
@@ -971,14 +976,13 @@ __device__ int fused_gen_item(const AttnArgs &a, int item, char *lds, int *s_lis
             write_row(a, cq, g * G + h, d, D, M, Ls, O);
         });
         }
-        if ((int)threadIdx.x < n_pairs && cell_active(a, c0 + threadIdx.x))
-            __hip_atomic_store(a.counters + (c0 + threadIdx.x) * a.Hkv + g, 0, __ATOMIC_RELAXED,
+        if ((int)threadIdx.x < n_pairs)
+            __hip_atomic_store(a.counters + (int)a.gorder[c0 + threadIdx.x] * a.Hkv + g, 0, __ATOMIC_RELAXED,
                                __HIP_MEMORY_SCOPE_AGENT);
         if (threadIdx.x == 0) s_list[0] = 0;   // nothing left to merge
     } else {
         waves_merge<D, G, NW>(S, lds, wpp, n_pairs, [&](int q, int h, int d, float M, float Lsum, f32x4_t O) {
-            if (!cell_active(a, c0 + q)) return;
-            const uint32_t slot = slot_off(a, c0 + q, g, a.n_p);
+            const uint32_t slot = slot_off(a, a.gorder[c0 + q], g, a.n_p);
             part_store4(r, slot + (uint32_t)(h * D + d) * 4u, O);
             if (d == 0) {
                 part_store1(r, slot + (uint32_t)(G * D + h) * 4u, M);
@@ -986,8 +990,8 @@ __device__ int fused_gen_item(const AttnArgs &a, int item, char *lds, int *s_lis
             }
         });
         stores_performed();
-        if ((int)threadIdx.x < n_pairs && cell_active(a, c0 + threadIdx.x) && arrive(a, c0 + threadIdx.x, g))
-            s_list[1 + atomicAdd(&s_list[0], 1)] = c0 + threadIdx.x;
+        if ((int)threadIdx.x < n_pairs && arrive(a, a.gorder[c0 + threadIdx.x], g))
+            s_list[1 + atomicAdd(&s_list[0], 1)] = a.gorder[c0 + threadIdx.x];
     }
     __syncthreads();
     return g;

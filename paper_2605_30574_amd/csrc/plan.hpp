@@ -297,7 +297,7 @@ inline AttnPlan plan_from_geo(const splice_shape &sh, const splice_call &call, c
     }
     if (bf16_path(sh)) {
         p.gen_pairs = gen_pairs(sh, p.geo.n_gen);
-        p.n_gen_items = ceil_div(sh.n_cells, p.gen_pairs) * sh.n_kv_heads;
+        p.n_gen_items = ceil_div(n_active, p.gen_pairs) * sh.n_kv_heads;   // active cells only
     } else {
         p.gen_pairs = 1;
         p.n_gen_items = sh.n_cells * sh.n_kv_heads * p.n_g;

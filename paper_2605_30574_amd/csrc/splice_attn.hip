@@ -42,6 +42,7 @@
 #include <stdint.h>
 #include <string.h>
 
+#include <algorithm>
 #include <mutex>
 
 #include "attn_kernels.hpp"
@@ -382,6 +383,24 @@ int32_t decode_attn_impl(const splice_shape *shape, const splice_call *call, con
         a.n_dormant = n - a.n_active;
     }
     for (int c = 0; c < SPLICE_MAX_CELLS; ++c) a.wfork[c] = forked && c < sh.n_cells ? cell_LW[2 * c + 1] : 0;
+    // generated-row items serve the cells with rows to stream (active, and
+    // diverged under a forked sweep), longest generated part first
+    {
+        int gen_len[SPLICE_MAX_CELLS];
+        int n_gc = 0;
+        for (int c = 0; c < sh.n_cells; ++c) {
+            const int s = step_of(c);
+            if (s < 0) continue;
+            splice_call cc = *call;
+            cc.step = s;
+            gen_len[c] = splice::geometry(sh, cc).n_gen;
+            a.gorder[n_gc++] = (uint8_t)c;
+        }
+        std::stable_sort(a.gorder, a.gorder + n_gc,
+                         [&](uint8_t x, uint8_t y) { return gen_len[x] > gen_len[y]; });
+        a.n_gen_cells = n_gc;
+        for (int i = n_gc; i < SPLICE_MAX_CELLS; ++i) a.gorder[i] = 0;
+    }
     for (; n < SPLICE_MAX_CELLS; ++n) a.order[n] = 0;
     if (splice::bf16_path(sh)) {
         a.n_rb = splice::row_groups(sh, a.n_clean, a.n_active);
