@@ -296,7 +296,7 @@ def stored_traffic(w_name: str):
     if fields.get("kernel_source_sha256_16") != kernel_source_hash():
         return None, "kernel changed since the counters were taken"
     try:
-        return float(fields["traffic_bytes_per_launch"]), path
+        return float(fields["traffic_bytes_per_launch"]), os.path.relpath(path, ROOT)
     except (KeyError, ValueError):
         return None, "malformed counter summary"
 
