@@ -22,7 +22,11 @@ struct AttnArgs {
     int C, Hq, Hkv, Tp, cap;
     int jp0, i0, n_gen, sa, sb;
     int zero_donor;
-    int n_p, p_len, n_g, g_len, n_slots, slot_floats;
+    int n_p, p_len, n_g, g_len, n_slots;
+    // partial-result region: the prompt slots [C][Hkv][n_p] of p_slot_bytes
+    // each, then from byte gen_base the generated-row slots [C][Hkv][n_g] of
+    // g_slot_bytes each
+    uint32_t p_slot_bytes, g_slot_bytes, gen_base;
     int n_rb, n_prompt_items, n_clean;
     int n_rg_clean;   // bf16 prompt row groups of unspliced cells (the rest: spliced cells)
     int wait_polls;   // bf16 generated-row items: most polls for the prompt partials
@@ -71,6 +75,71 @@ __device__ __forceinline__ f32x4_t part_load4(__amdgpu_buffer_rsrc_t r, uint32_t
 }
 __device__ __forceinline__ float part_load1(__amdgpu_buffer_rsrc_t r, uint32_t off) {
     return __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(r, off, 0, kSc1));
+}
+
+// fp16 partial values (converted from fp32 rounding to nearest even): four
+// outputs in 8 bytes, or a group of eight in 16.
+typedef _Float16 h16x4_t __attribute__((ext_vector_type(4)));
+typedef _Float16 h16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x8_t __attribute__((ext_vector_type(8)));
+__device__ __forceinline__ f32x4_t part_load4h(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+    const u32x2_t w = __builtin_amdgcn_raw_buffer_load_b64(r, off, 0, kSc1);
+    return __builtin_convertvector(__builtin_bit_cast(h16x4_t, w), f32x4_t);
+}
+
+// One partial-result slot of a (cell, KV head): o[G][D], then m[G] and l[G]
+// in fp32.  A 16-bit slot (the prompt chunks of a bf16 call) holds
+// o / (l sc) in fp16 and adds w[G] = l sc, the weight its o enters the merge
+// with; sc is a power of two, 1 unless the largest |o / l| of the row is
+// above kH16Limit.  Since o / l is a convex combination of V rows, the
+// stored values are bounded by the largest |v| of the chunk.
+//
+// A 16-bit row is stored in groups of eight values, d0 .. d0 + 3 and
+// d0 + 16 .. d0 + 19 for d0 = 32 u + 4 q (q < 4), at group 4 u + q: the
+// outputs one lane of a prompt item holds for two adjacent 16-row MFMA
+// tiles, so the lane writes a group with one 16-byte store and a reader of
+// 8 outputs loads it with one.  o(h, d) is the byte offset of the four
+// outputs d .. d + 3 (d a multiple of 4).
+template <int D, int G, bool H16>
+struct Slot {
+    static constexpr uint32_t OE = H16 ? 2 : 4;
+    static constexpr uint32_t ML = (uint32_t)(G * D) * OE;
+    __device__ static uint32_t o(int h, int d) {
+        if constexpr (H16) {
+            const int t = d >> 4, u = t >> 1, hf = t & 1, q = (d & 15) >> 2;
+            return (uint32_t)(h * D) * 2u + (uint32_t)((u * 4 + q) * 16 + hf * 8);
+        } else {
+            return (uint32_t)(h * D + d) * 4u;
+        }
+    }
+    __device__ static uint32_t m(int h) { return ML + 4u * (uint32_t)h; }
+    __device__ static uint32_t l(int h) { return ML + 4u * (uint32_t)(G + h); }
+    __device__ static uint32_t w(int h) { return ML + 4u * (uint32_t)(2 * G + h); }
+};
+constexpr float kH16Limit = 32768.f;
+
+// Byte offsets of prompt slot k and generated-row slot j of (cell c, KV head g).
+__device__ __forceinline__ uint32_t pslot_off(const AttnArgs &a, int c, int g, int k) {
+    return ((uint32_t)(c * a.Hkv + g) * (uint32_t)a.n_p + (uint32_t)k) * a.p_slot_bytes;
+}
+__device__ __forceinline__ uint32_t gslot_off(const AttnArgs &a, int c, int g, int j) {
+    return a.gen_base + ((uint32_t)(c * a.Hkv + g) * (uint32_t)a.n_g + (uint32_t)j) * a.g_slot_bytes;
+}
+
+// (o, m, l, w) of four outputs of a prompt slot at byte offset base.
+template <int D, int G, bool H16>
+__device__ __forceinline__ void load_pslot(__amdgpu_buffer_rsrc_t r, uint32_t base, int h, int d, f32x4_t &o,
+                                           float &m, float &l, float &w) {
+    using SL = Slot<D, G, H16>;
+    if constexpr (H16) {
+        o = part_load4h(r, base + SL::o(h, d));
+        w = part_load1(r, base + SL::w(h));
+    } else {
+        o = part_load4(r, base + SL::o(h, d));
+    }
+    m = part_load1(r, base + SL::m(h));
+    l = part_load1(r, base + SL::l(h));
+    if constexpr (!H16) w = l;
 }
 
 // ---------------------------------------------------------- vector-ALU rows
@@ -310,11 +379,6 @@ __device__ __forceinline__ void valu_store_partial(const AttnArgs &a, float (&m)
     });
 }
 
-// Byte offset of slot k of (cell c, KV head g) in the partial region.
-__device__ __forceinline__ uint32_t slot_off(const AttnArgs &a, int c, int g, int k) {
-    return (uint32_t)((((c * a.Hkv + g) * a.n_slots) + k) * a.slot_floats) * 4u;
-}
-
 // Generated rows of one (cell, KV head): contiguous, never spliced.
 template <int D, int G, bool BF16>
 __device__ void gen_item(const AttnArgs &a, int c, int g, int gk, char *buf) {
@@ -333,7 +397,7 @@ __device__ void gen_item(const AttnArgs &a, int c, int g, int gk, char *buf) {
                                 return true;
                             },
                             m, l, o);
-    valu_store_partial<D, G, BF16>(a, m, l, o, buf, slot_off(a, c, g, a.n_p + gk));
+    valu_store_partial<D, G, BF16>(a, m, l, o, buf, gslot_off(a, c, g, gk));
 }
 
 // Prompt chunk of one (cell, KV head) on the vector ALUs (f32 inputs): each
@@ -359,7 +423,7 @@ __device__ void prompt_item_valu(const AttnArgs &a, int c, int g, int pk, char *
                                 return !(spl && in_span && a.zero_donor);
                             },
                             m, l, o);
-    valu_store_partial<D, G, BF16>(a, m, l, o, buf, slot_off(a, c, g, pk));
+    valu_store_partial<D, G, BF16>(a, m, l, o, buf, pslot_off(a, c, g, pk));
 }
 
 // ----------------------------------------------------------- merging
@@ -398,6 +462,23 @@ __device__ __forceinline__ void fold_slot(float mk, float lk, f32x4_t ok, float 
     O.y = fmaf(ok.y, f, O.y);
     O.z = fmaf(ok.z, f, O.z);
     O.w = fmaf(ok.w, f, O.w);
+}
+
+// A prompt slot: l enters with 2^(m - M), o with w 2^(m - M) (a 16-bit slot
+// holds o / w); an fp32 slot has w = l and folds exactly as fold_slot.
+template <bool H16>
+__device__ __forceinline__ void fold_pslot(float mk, float lk, float wk, f32x4_t ok, float M, float &L, f32x4_t &O) {
+    if constexpr (H16) {
+        const float f = fast_exp2(mk - M);
+        L = fmaf(lk, f, L);
+        const float fw = wk * f;
+        O.x = fmaf(ok.x, fw, O.x);
+        O.y = fmaf(ok.y, fw, O.y);
+        O.z = fmaf(ok.z, fw, O.z);
+        O.w = fmaf(ok.w, fw, O.w);
+    } else {
+        fold_slot(mk, lk, ok, M, L, O);
+    }
 }
 
 // What cell c sees: its step, visible generated rows [i0, i0 + n_gen), first
@@ -454,36 +535,56 @@ __device__ __forceinline__ void write_row(const AttnArgs &a, int c, int hq, int 
 // groups of four consecutive outputs and loads them two slots at a time.
 constexpr int kMergeUnits = 4;
 
-template <int D, int G, int NT>
+template <int D, int G, int NT, bool H16>
 __device__ void combine_cells(const AttnArgs &a, const int *list, int n, int g, char *buf) {
+    using SP = Slot<D, G, H16>;     // prompt slots
+    using SG = Slot<D, G, false>;   // generated-row slots
     const __amdgpu_buffer_rsrc_t r = part_rsrc(a);
     float *s_m = reinterpret_cast<float *>(buf);           // [n][n_slots][G]
     float *s_l = s_m + kRowBlock * kMaxSlots;               // [n][n_slots][G]
+    float *s_w = H16 ? s_l + kRowBlock * kMaxSlots : s_l;  // [n][n_slots][G]: weights of o (H16 only)
     const int per_cell = a.n_slots * G;
     for (int t = threadIdx.x; t < n * per_cell; t += NT) {
         const int i = t / per_cell, rem = t % per_cell;
         const int k = rem / G, h = rem % G;
-        const uint32_t slot = slot_off(a, list[i], g, k);
-        s_m[t] = part_load1(r, slot + (uint32_t)(G * D + h) * 4u);
-        s_l[t] = part_load1(r, slot + (uint32_t)(G * D + G + h) * 4u);
+        if (k < a.n_p) {
+            const uint32_t slot = pslot_off(a, list[i], g, k);
+            s_m[t] = part_load1(r, slot + SP::m(h));
+            s_l[t] = part_load1(r, slot + SP::l(h));
+            if constexpr (H16) s_w[t] = part_load1(r, slot + SP::w(h));
+        } else {
+            const uint32_t slot = gslot_off(a, list[i], g, k - a.n_p);
+            s_m[t] = part_load1(r, slot + SG::m(h));
+            s_l[t] = part_load1(r, slot + SG::l(h));
+            if constexpr (H16) s_w[t] = 1.f;   // fp32 slot: o itself, weight 2^(m - M)
+        }
     }
     __syncthreads();
     constexpr int UPC = G * D / 4;                           // 4-wide units per cell
     const int total = n * UPC;
-    const uint32_t slot_bytes = (uint32_t)a.slot_floats * 4u;
+    // slot k of unit b: its four outputs, in the slot's own format
+    auto load_o = [&](int c, int h, int d, int k) -> f32x4_t {
+        if (k < a.n_p) {
+            const uint32_t off = pslot_off(a, c, g, k) + SP::o(h, d);
+            if constexpr (H16) return part_load4h(r, off);
+            else return part_load4(r, off);
+        }
+        return part_load4(r, gslot_off(a, c, g, k - a.n_p) + SG::o(h, d));
+    };
     for (int u0 = threadIdx.x; u0 < total; u0 += NT * kMergeUnits) {
         float M[kMergeUnits], L[kMergeUnits];
         f32x4_t O[kMergeUnits];
-        uint32_t base[kMergeUnits];
+        int cb[kMergeUnits], hb[kMergeUnits], db[kMergeUnits];
         int sm_off[kMergeUnits];
 #pragma unroll
         for (int b = 0; b < kMergeUnits; ++b) {
             const int u = min(u0 + b * NT, total - 1);   // tail units repeat a valid one
             const int i = u / UPC, rem = u % UPC;
-            const int h = rem / (D / 4), d = 4 * (rem % (D / 4));
+            hb[b] = rem / (D / 4);
+            db[b] = 4 * (rem % (D / 4));
             const int c = list[i];
-            sm_off[b] = i * per_cell + h;
-            base[b] = slot_off(a, c, g, 0) + (uint32_t)(h * D + d) * 4u;
+            cb[b] = c;
+            sm_off[b] = i * per_cell + hb[b];
             const bool zero_term = has_zero_term(a, c);
             float mx = zero_term ? 0.f : -INFINITY;
             for (int k = 0; k < a.n_slots; ++k) mx = fmaxf(mx, s_m[sm_off[b] + k * G]);
@@ -496,22 +597,25 @@ __device__ void combine_cells(const AttnArgs &a, const int *list, int n, int g, 
             f32x4_t v0[kMergeUnits], v1[kMergeUnits];
 #pragma unroll
             for (int b = 0; b < kMergeUnits; ++b) {
-                v0[b] = part_load4(r, base[b] + (uint32_t)k * slot_bytes);
-                v1[b] = part_load4(r, base[b] + (uint32_t)(k + 1) * slot_bytes);
+                v0[b] = load_o(cb[b], hb[b], db[b], k);
+                v1[b] = load_o(cb[b], hb[b], db[b], k + 1);
             }
 #pragma unroll
             for (int b = 0; b < kMergeUnits; ++b) {
-                fold_slot(s_m[sm_off[b] + k * G], s_l[sm_off[b] + k * G], v0[b], M[b], L[b], O[b]);
-                fold_slot(s_m[sm_off[b] + (k + 1) * G], s_l[sm_off[b] + (k + 1) * G], v1[b], M[b], L[b], O[b]);
+                const int s0 = sm_off[b] + k * G, s1 = sm_off[b] + (k + 1) * G;
+                fold_pslot<H16>(s_m[s0], s_l[s0], s_w[s0], v0[b], M[b], L[b], O[b]);
+                fold_pslot<H16>(s_m[s1], s_l[s1], s_w[s1], v1[b], M[b], L[b], O[b]);
             }
         }
         if (k < a.n_slots) {
             f32x4_t v0[kMergeUnits];
 #pragma unroll
-            for (int b = 0; b < kMergeUnits; ++b) v0[b] = part_load4(r, base[b] + (uint32_t)k * slot_bytes);
+            for (int b = 0; b < kMergeUnits; ++b) v0[b] = load_o(cb[b], hb[b], db[b], k);
 #pragma unroll
-            for (int b = 0; b < kMergeUnits; ++b)
-                fold_slot(s_m[sm_off[b] + k * G], s_l[sm_off[b] + k * G], v0[b], M[b], L[b], O[b]);
+            for (int b = 0; b < kMergeUnits; ++b) {
+                const int s0 = sm_off[b] + k * G;
+                fold_pslot<H16>(s_m[s0], s_l[s0], s_w[s0], v0[b], M[b], L[b], O[b]);
+            }
         }
 #pragma unroll
         for (int b = 0; b < kMergeUnits; ++b) {
@@ -569,7 +673,7 @@ __global__ __launch_bounds__(kThreads) void items_kernel(AttnArgs a) {
         s_list[1] = c;
     }
     __syncthreads();
-    if (s_list[0]) combine_cells<D, G, kThreads>(a, s_list + 1, 1, g, buf);
+    if (s_list[0]) combine_cells<D, G, kThreads, false>(a, s_list + 1, 1, g, buf);
 }
 
 // ------------------------------------------------------- bf16, long prompts
@@ -613,22 +717,14 @@ struct Fused {
 // The prompt slots 0 .. n_p - 1 (n_p <= B) of one (row, four outputs) in one
 // round of loads: M over the slots and this item's own maximum Mg, the ZERO
 // term, then the slots folded in order (the fixed fold order).
-template <int B>
-__device__ __forceinline__ void merge_slots_once(const AttnArgs &a, __amdgpu_buffer_rsrc_t r, uint32_t sbase,
-                                                 uint32_t slot_bytes, uint32_t o_off, uint32_t m_off,
-                                                 uint32_t l_off, int nz, float Mg, float &M, float &Ls,
-                                                 f32x4_t &O) {
+template <int D, int G, int B>
+__device__ __forceinline__ void merge_slots_once(const AttnArgs &a, __amdgpu_buffer_rsrc_t r, uint32_t sbase, int h,
+                                                 int d, int nz, float Mg, float &M, float &Ls, f32x4_t &O) {
     f32x4_t ok[B];
-    float mk[B], lk[B];
+    float mk[B], lk[B], wk[B];
 #pragma unroll
-    for (int j = 0; j < B; ++j) {
-        if (j < a.n_p) {
-            const uint32_t off = sbase + (uint32_t)j * slot_bytes;
-            ok[j] = part_load4(r, off + o_off);
-            mk[j] = part_load1(r, off + m_off);
-            lk[j] = part_load1(r, off + l_off);
-        }
-    }
+    for (int j = 0; j < B; ++j)
+        if (j < a.n_p) load_pslot<D, G, true>(r, sbase + (uint32_t)j * a.p_slot_bytes, h, d, ok[j], mk[j], lk[j], wk[j]);
 #pragma unroll
     for (int j = 0; j < B; ++j)
         if (j < a.n_p) M = fmaxf(M, mk[j]);
@@ -636,7 +732,7 @@ __device__ __forceinline__ void merge_slots_once(const AttnArgs &a, __amdgpu_buf
     if (nz > 0) Ls = (float)nz * fast_exp2(-M);
 #pragma unroll
     for (int j = 0; j < B; ++j)
-        if (j < a.n_p) fold_slot(mk[j], lk[j], ok[j], M, Ls, O);
+        if (j < a.n_p) fold_pslot<true>(mk[j], lk[j], wk[j], ok[j], M, Ls, O);
 }
 
 template <int D, int G>
@@ -645,7 +741,7 @@ struct FusedLds {
     static constexpr int PROMPT = Direct<D>::LDS;
     static constexpr int WAVE_MERGE = NW * G * (D + 2) * 4;                     // waves_merge buffer
     static constexpr int GEN = cmax(NW * WaveMfma<D>::LDS, WAVE_MERGE);         // V^T tiles, wave merge
-    static constexpr int MERGE = 2 * kRowBlock * kMaxSlots * 4;                 // combine_cells staging
+    static constexpr int MERGE = 3 * kRowBlock * kMaxSlots * 4;                 // combine_cells staging (m, l, w)
     static constexpr int BYTES = cmax(cmax(PROMPT, GEN), MERGE);
     static_assert(BYTES <= 160 * 1024 - 4096, "fits the LDS of a compute unit");
 };
@@ -718,19 +814,36 @@ __device__ int fused_prompt_item(const AttnArgs &a, int item, char *lds, int *s_
     });
     direct_stream<D, RB, Fused<D>::NW>(L, qrow, a.qk_scale, a.row_lo != 0, lo, lds, S);
 
+    // each row's partial as a 16-bit slot: o / (l sc) in fp16, m, l, w = l sc
+    using SL = Slot<D, G, true>;
     const __amdgpu_buffer_rsrc_t r = part_rsrc(a);
     static_for<0, RB>([&](auto rb) {
         float l = S.lsum[rb];
         l += __shfl_xor(l, 16);
         l += __shfl_xor(l, 32);
+        float amax = 0.f;
+        static_for<0, X::NDT>([&](auto t) {
+            static_for<0, 4>([&](auto i) { amax = fmaxf(amax, fabsf(S.o[rb][t][(int)i])); });
+        });
+        amax = fmaxf(amax, __shfl_xor(amax, 16));
+        amax = fmaxf(amax, __shfl_xor(amax, 32));
+        const float inv_l = l > 0.f ? 1.f / l : 0.f;
+        const float big = amax * inv_l;
+        const float sc = big > kH16Limit ? exp2f(ceilf(log2f(big / kH16Limit))) : 1.f;
+        const float mul = inv_l / sc;
         if (ok[rb]) {
-            const uint32_t slot = slot_off(a, cell[rb], g, pk);
-            static_for<0, X::NDT>([&](auto t) {
-                part_store4(r, slot + (uint32_t)(hh[rb] * D + 16 * t + 4 * quad) * 4u, S.o[rb][t]);
+            const uint32_t slot = pslot_off(a, cell[rb], g, pk);
+            static_for<0, X::NDT / 2>([&](auto u) {
+                const f32x4_t lo = S.o[rb][2 * u] * mul, hi = S.o[rb][2 * u + 1] * mul;
+                const h16x8_t h = __builtin_convertvector(
+                    (f32x8_t{lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w}), h16x8_t);
+                __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4_t, h), r,
+                                                       slot + SL::o(hh[rb], 32 * u + 4 * quad), 0, kSc1);
             });
             if (quad == 0) {
-                part_store1(r, slot + (uint32_t)(G * D + hh[rb]) * 4u, S.m[rb]);
-                part_store1(r, slot + (uint32_t)(G * D + G + hh[rb]) * 4u, l);
+                part_store1(r, slot + SL::m(hh[rb]), S.m[rb]);
+                part_store1(r, slot + SL::l(hh[rb]), l);
+                part_store1(r, slot + SL::w(hh[rb]), l * sc);
             }
         }
     });
@@ -748,20 +861,22 @@ __device__ int fused_prompt_item(const AttnArgs &a, int item, char *lds, int *s_
 
 // In-place merge of a generated-row item whose cells' prompt partials are
 // all stored: the item's own partial (its waves combined through LDS) is
-// the last slot and never leaves the chip.  Each thread owns up to U units
-// (cell, q head, four outputs) per round; the loads of every prompt slot of
-// a round's units are issued before the waves' partials are combined, so
-// their latency overlaps the LDS work.  Fold order (fixed, as in
-// combine_cells): the ZERO term, the prompt slots in order, this item's
-// slot.
+// the last slot and never leaves the chip.  A unit is eight outputs of one
+// (cell, q head), d0 .. d0 + 3 and d0 + 16 .. d0 + 19: one 16-byte load per
+// prompt slot.  Each thread owns up to U units per round; the loads of
+// every prompt slot of a round's units are issued before the waves'
+// partials are combined, so their latency overlaps the LDS work.  Fold
+// order (fixed, as in combine_cells): the ZERO term, the prompt slots in
+// order, this item's slot; each output is folded exactly as there.
 template <int D, int G, int NW, int B, int U>
 __device__ __forceinline__ void gen_merge_in_place(const AttnArgs &a, const WaveState<D> &S, char *buf, int wpp,
                                                    int n_pairs, int c0, int g) {
     using W = WaveMfma<D>;
+    using SL = Slot<D, G, true>;
     constexpr int NT = NW * 64;
-    constexpr int UPG = G * D / 4;   // units of four outputs per (cell, KV head)
+    constexpr int UPR = D / 8;       // units per (cell, q head)
+    constexpr int UPG = G * UPR;     // units per (cell, KV head)
     const __amdgpu_buffer_rsrc_t r = part_rsrc(a);
-    const uint32_t slot_bytes = (uint32_t)a.slot_floats * 4u;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int col = lane & 15, quad = lane >> 4;
     const int total = n_pairs * UPG;
@@ -779,24 +894,24 @@ __device__ __forceinline__ void gen_merge_in_place(const AttnArgs &a, const Wave
         }
     }
     for (int e0 = 0; e0 < total; e0 += NT * U) {
-        f32x4_t ok[U][B];
-        float mk[U][B], lk[U][B];
+        u32x4_t ok[U][B];   // eight fp16 outputs
+        float mk[U][B], lk[U][B], wk[U][B];
         int pe[U], he[U], de[U];
         static_for<0, U>([&](auto u) {
             const int e = min(e0 + (int)u * NT + tid, total - 1);   // past the end: repeat a valid unit
             pe[u] = e / UPG;
-            he[u] = (e % UPG) / (D / 4);
-            de[u] = 4 * (e % (D / 4));
-            const uint32_t sbase = slot_off(a, a.gorder[c0 + pe[u]], g, 0);
-            const uint32_t o_off = (uint32_t)(he[u] * D + de[u]) * 4u;
-            const uint32_t m_off = (uint32_t)(G * D + he[u]) * 4u, l_off = (uint32_t)(G * D + G + he[u]) * 4u;
+            he[u] = (e % UPG) / UPR;
+            const int r8 = e % UPR;
+            de[u] = 32 * (r8 >> 2) + 4 * (r8 & 3);
+            const uint32_t sbase = pslot_off(a, a.gorder[c0 + pe[u]], g, 0);
 #pragma unroll
             for (int j = 0; j < B; ++j) {
                 if (j < a.n_p) {
-                    const uint32_t off = sbase + (uint32_t)j * slot_bytes;
-                    ok[u][j] = part_load4(r, off + o_off);
-                    mk[u][j] = part_load1(r, off + m_off);
-                    lk[u][j] = part_load1(r, off + l_off);
+                    const uint32_t off = sbase + (uint32_t)j * a.p_slot_bytes;
+                    ok[u][j] = __builtin_amdgcn_raw_buffer_load_b128(r, off + SL::o(he[u], de[u]), 0, kSc1);
+                    mk[u][j] = part_load1(r, off + SL::m(he[u]));
+                    lk[u][j] = part_load1(r, off + SL::l(he[u]));
+                    wk[u][j] = part_load1(r, off + SL::w(he[u]));
                 }
             }
         });
@@ -805,7 +920,7 @@ __device__ __forceinline__ void gen_merge_in_place(const AttnArgs &a, const Wave
             const int e = e0 + (int)u * NT + tid;
             const int cq = a.gorder[c0 + pe[u]];
             if (e < total) {
-                const int h = he[u], d = de[u], w0 = pe[u] * wpp;
+                const int h = he[u], d0 = de[u], d1 = d0 + 16, w0 = pe[u] * wpp;
                 // this item's partial: its waves combined
                 float Mg = -INFINITY;
 #pragma unroll
@@ -813,14 +928,15 @@ __device__ __forceinline__ void gen_merge_in_place(const AttnArgs &a, const Wave
                     if (i < wpp) Mg = fmaxf(Mg, s_m[(w0 + i) * G + h]);
                 const float Mgs = Mg == -INFINITY ? 0.f : Mg;
                 float Lg = 0.f;
-                f32x4_t Og = {0.f, 0.f, 0.f, 0.f};
+                f32x4_t Og0 = {0.f, 0.f, 0.f, 0.f}, Og1 = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
                 for (int i = 0; i < NW; ++i) {
                     if (i < wpp) {
                         const int w = w0 + i;
                         const float f = fast_exp2(s_m[w * G + h] - Mgs);
                         Lg = fmaf(s_l[w * G + h], f, Lg);
-                        Og += *reinterpret_cast<const f32x4_t *>(s_o + (w * G + h) * D + d) * f;
+                        Og0 += *reinterpret_cast<const f32x4_t *>(s_o + (w * G + h) * D + d0) * f;
+                        Og1 += *reinterpret_cast<const f32x4_t *>(s_o + (w * G + h) * D + d1) * f;
                     }
                 }
                 const int nz = zero_slots(a, cq);
@@ -829,13 +945,20 @@ __device__ __forceinline__ void gen_merge_in_place(const AttnArgs &a, const Wave
                 for (int j = 0; j < B; ++j)
                     if (j < a.n_p) M = fmaxf(M, mk[u][j]);
                 M = fmaxf(M, Mg);
-                float Ls = nz > 0 ? (float)nz * fast_exp2(-M) : 0.f;
-                f32x4_t O = {0.f, 0.f, 0.f, 0.f};
+                float Ls = nz > 0 ? (float)nz * fast_exp2(-M) : 0.f, Ls1 = Ls;
+                f32x4_t O0 = {0.f, 0.f, 0.f, 0.f}, O1 = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-                for (int j = 0; j < B; ++j)
-                    if (j < a.n_p) fold_slot(mk[u][j], lk[u][j], ok[u][j], M, Ls, O);
-                fold_slot(Mg, Lg, Og, M, Ls, O);   // this item's slot, a.n_p, comes last
-                write_row(a, cq, g * G + h, d, D, M, Ls, O);
+                for (int j = 0; j < B; ++j) {
+                    if (j < a.n_p) {
+                        const f32x8_t v = __builtin_convertvector(__builtin_bit_cast(h16x8_t, ok[u][j]), f32x8_t);
+                        fold_pslot<true>(mk[u][j], lk[u][j], wk[u][j], f32x4_t{v[0], v[1], v[2], v[3]}, M, Ls, O0);
+                        fold_pslot<true>(mk[u][j], lk[u][j], wk[u][j], f32x4_t{v[4], v[5], v[6], v[7]}, M, Ls1, O1);
+                    }
+                }
+                fold_slot(Mg, Lg, Og0, M, Ls, O0);   // this item's slot, a.n_p, comes last
+                fold_slot(Mg, Lg, Og1, M, Ls1, O1);
+                write_row(a, cq, g * G + h, d0, D, M, Ls, O0);
+                write_row(a, cq, g * G + h, d1, D, M, Ls1, O1);
             }
         });
     }
@@ -932,44 +1055,38 @@ __device__ int fused_gen_item(const AttnArgs &a, int item, char *lds, int *s_lis
     __syncthreads();   // also: every wave is done with its V^T tile
     const bool ready = s_list[0] < 0;
     const __amdgpu_buffer_rsrc_t r = part_rsrc(a);
-    const uint32_t slot_bytes = (uint32_t)a.slot_floats * 4u;
     if (ready) {
         if (a.n_p <= 8) {
-            gen_merge_in_place<D, G, NW, 8, 2>(a, S, lds, wpp, n_pairs, c0, g);
-        } else if (a.n_p <= 16) {
-            gen_merge_in_place<D, G, NW, 16, 1>(a, S, lds, wpp, n_pairs, c0, g);
+            gen_merge_in_place<D, G, NW, 8, 1>(a, S, lds, wpp, n_pairs, c0, g);
         } else {
         waves_merge<D, G, NW>(S, lds, wpp, n_pairs, [&](int q, int h, int d, float Mg, float Lg, f32x4_t Og) {
             const int cq = a.gorder[c0 + q];
-            const uint32_t sbase = slot_off(a, cq, g, 0);
-            const uint32_t o_off = (uint32_t)(h * D + d) * 4u;
-            const uint32_t m_off = (uint32_t)(G * D + h) * 4u, l_off = (uint32_t)(G * D + G + h) * 4u;
+            const uint32_t sbase = pslot_off(a, cq, g, 0);
             const int nz = zero_slots(a, cq);
             float M = nz > 0 ? 0.f : -INFINITY;
             float Ls = 0.f;
             f32x4_t O = {0.f, 0.f, 0.f, 0.f};
             if (a.n_p <= 8) {
-                merge_slots_once<8>(a, r, sbase, slot_bytes, o_off, m_off, l_off, nz, Mg, M, Ls, O);
+                merge_slots_once<D, G, 8>(a, r, sbase, h, d, nz, Mg, M, Ls, O);
             } else if (a.n_p <= 16) {
-                merge_slots_once<16>(a, r, sbase, slot_bytes, o_off, m_off, l_off, nz, Mg, M, Ls, O);
+                merge_slots_once<D, G, 16>(a, r, sbase, h, d, nz, Mg, M, Ls, O);
             } else {
+                using SL = Slot<D, G, true>;
                 constexpr int B = 8;
-                for (int k = 0; k < a.n_p; ++k) M = fmaxf(M, part_load1(r, sbase + (uint32_t)k * slot_bytes + m_off));
+                for (int k = 0; k < a.n_p; ++k)
+                    M = fmaxf(M, part_load1(r, sbase + (uint32_t)k * a.p_slot_bytes + SL::m(h)));
                 M = fmaxf(M, Mg);
                 if (nz > 0) Ls = (float)nz * fast_exp2(-M);
                 for (int k0 = 0; k0 < a.n_p; k0 += B) {
                     f32x4_t ok[B];
-                    float mk[B], lk[B];
-#pragma unroll
-                    for (int j = 0; j < B; ++j) {
-                        const uint32_t off = sbase + (uint32_t)min(k0 + j, a.n_p - 1) * slot_bytes;
-                        ok[j] = part_load4(r, off + o_off);
-                        mk[j] = part_load1(r, off + m_off);
-                        lk[j] = part_load1(r, off + l_off);
-                    }
+                    float mk[B], lk[B], wk[B];
 #pragma unroll
                     for (int j = 0; j < B; ++j)
-                        if (k0 + j < a.n_p) fold_slot(mk[j], lk[j], ok[j], M, Ls, O);
+                        load_pslot<D, G, true>(r, sbase + (uint32_t)min(k0 + j, a.n_p - 1) * a.p_slot_bytes, h, d, ok[j],
+                                               mk[j], lk[j], wk[j]);
+#pragma unroll
+                    for (int j = 0; j < B; ++j)
+                        if (k0 + j < a.n_p) fold_pslot<true>(mk[j], lk[j], wk[j], ok[j], M, Ls, O);
                 }
             }
             fold_slot(Mg, Lg, Og, M, Ls, O);   // this item's slot, a.n_p, comes last
@@ -982,11 +1099,12 @@ __device__ int fused_gen_item(const AttnArgs &a, int item, char *lds, int *s_lis
         if (threadIdx.x == 0) s_list[0] = 0;   // nothing left to merge
     } else {
         waves_merge<D, G, NW>(S, lds, wpp, n_pairs, [&](int q, int h, int d, float M, float Lsum, f32x4_t O) {
-            const uint32_t slot = slot_off(a, a.gorder[c0 + q], g, a.n_p);
-            part_store4(r, slot + (uint32_t)(h * D + d) * 4u, O);
+            using SG = Slot<D, G, false>;
+            const uint32_t slot = gslot_off(a, a.gorder[c0 + q], g, 0);
+            part_store4(r, slot + SG::o(h, d), O);
             if (d == 0) {
-                part_store1(r, slot + (uint32_t)(G * D + h) * 4u, M);
-                part_store1(r, slot + (uint32_t)(G * D + G + h) * 4u, Lsum);
+                part_store1(r, slot + SG::m(h), M);
+                part_store1(r, slot + SG::l(h), Lsum);
             }
         });
         stores_performed();
@@ -1013,7 +1131,7 @@ void fused_kernel(AttnArgs a) {
     // merge in batches whose (m, l) staging fits
     const int per = max(1, (kRowBlock * kMaxSlots) / (a.n_slots * G));
     for (int i = 0; i < n; i += per) {
-        combine_cells<D, G, Fused<D>::NT>(a, s_list + 1 + i, min(per, n - i), g, lds);
+        combine_cells<D, G, Fused<D>::NT, true>(a, s_list + 1 + i, min(per, n - i), g, lds);
         __syncthreads();
     }
 }

@@ -145,6 +145,14 @@ inline int slot_floats(int G, int D) { return (G * D + 2 * G + 63) / 64 * 64; }
 
 inline bool bf16_path(const splice_shape &sh) { return sh.dtype == SPLICE_BF16; }
 
+// Bytes per prompt slot: an fp32 slot, or for bf16 inputs a 16-bit one
+// (o[G][D] in fp16, then m[G], l[G] and the weights w[G] in fp32, padded to
+// 256 bytes), never larger than an fp32 slot.
+inline int prompt_slot_bytes(const splice_shape &sh) {
+    const int G = group_of(sh), D = sh.head_dim;
+    return bf16_path(sh) ? round_up((int64_t)G * D * 2 + 12 * G, 256) : slot_floats(G, D) * 4;
+}
+
 // bf16 row groups of one KV head: the rows of unspliced cells and the rows
 // of spliced cells are grouped separately (group_rows(D) rows per group), so
 // no group needs both the clean and the donor span.  n_clean of the call's
@@ -336,8 +344,10 @@ struct WorkspaceLayout {
 // wait ran out, counted since splice_workspace_init.
 constexpr size_t kStatsBytes = 256;
 
-// Statistics, counters [C][Hkv] (int32), then one partial slot per (cell,
-// KV head, chunk).
+// Statistics, counters [C][Hkv] (int32), then the partial results: the
+// region is sized for one fp32 slot per (cell, KV head, chunk), which also
+// holds a bf16 call's smaller prompt slots followed by its generated-row
+// slots.
 inline WorkspaceLayout workspace_layout(const splice_shape &sh, int n_slots) {
     WorkspaceLayout w;
     const int64_t pairs = (int64_t)sh.n_cells * sh.n_kv_heads;

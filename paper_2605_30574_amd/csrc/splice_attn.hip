@@ -354,7 +354,10 @@ int32_t decode_attn_impl(const splice_shape *shape, const splice_call *call, con
     a.zero_donor = zero ? 1 : 0;
     a.n_p = plan.n_p; a.p_len = plan.p_len; a.n_g = plan.n_g; a.g_len = plan.g_len;
     a.n_slots = plan.n_slots;
-    a.slot_floats = splice::slot_floats(G, sh.head_dim);
+    // prompt slots [C][Hkv][n_p], then generated-row slots [C][Hkv][n_g]
+    a.p_slot_bytes = (uint32_t)splice::prompt_slot_bytes(sh);
+    a.g_slot_bytes = (uint32_t)splice::slot_floats(G, sh.head_dim) * 4u;
+    a.gen_base = (uint32_t)((int64_t)sh.n_cells * sh.n_kv_heads * plan.n_p * a.p_slot_bytes);
     a.n_rb = 0; a.n_rg_clean = 0;
     a.n_prompt_items = plan.n_prompt_items;
     a.gen_pairs = plan.gen_pairs;

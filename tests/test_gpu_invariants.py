@@ -101,6 +101,34 @@ def test_merge_site_does_not_change_bits(donor):
             assert 0 <= n <= pairs
 
 
+@pytest.mark.parametrize("merge_wait", [0, -1])
+def test_large_values_scale_exactly(merge_wait):
+    """V scaled by 2^17 scales out by 2^17 and leaves lse as it was: every
+    product and sum of P.V moves by a power of two, and a prompt partial of
+    a bf16 call, kept in fp16 as o / (l sc), takes a power-of-two range
+    factor sc once the row's largest |o / l| passes the fp16 limit (here it
+    does: |v| reaches about 5 * 2^17), so its rounding moves with the scale
+    too.  The only slack allowed is for partial values below the fp16
+    normal range at scale 1, which are kept more precisely at 2^17.  Both
+    merge sites (in place, and the hand-over merge) read such slots."""
+    w = _w()
+    lw = workloads.cell_lw(w)
+    layer, step = 1, 150
+    bufs = gc.gpu_layer(w, layer)
+    f = float(2 ** 17)
+    big = dict(bufs, clean_v=bufs["clean_v"] * f, donor_v=bufs["donor_v"] * f, gen_v=bufs["gen_v"] * f)
+    assert torch.equal(big["gen_v"] / f, bufs["gen_v"])   # the scaling itself is exact in bf16
+    q = workloads.make_q(w, layer, step, device="cuda")
+    gc.announce(f"scale 2^17 merge_wait={merge_wait}")
+    o, l = gc.run_attn(w, layer, step, bufs, q, lw, split=64, merge_wait=merge_wait)
+    ob, lb = gc.run_attn(w, layer, step, big, q, lw, split=64, merge_wait=merge_wait)
+    assert np.all(np.isfinite(ob)) and np.array_equal(l, lb)
+    assert np.abs(ob / f - o).max() <= 1e-6 * max(1.0, np.abs(o).max())
+    hb = gc.host(big)
+    ref_o, ref_l = gc.run_oracle(w, layer, step, hb, workloads.to_numpy(q), lw)
+    gc.assert_attn_close(ob / f, lb, ref_o / f, ref_l, "V x 2^17")
+
+
 def test_split_changes_only_rounding():
     w = _w()
     lw = workloads.cell_lw(w)
