@@ -89,10 +89,11 @@ __device__ __forceinline__ f32x4_t part_load4h(__amdgpu_buffer_rsrc_t r, uint32_
 
 // One partial-result slot of a (cell, KV head): o[G][D], then m[G] and l[G]
 // in fp32.  A 16-bit slot (the prompt chunks of a bf16 call) holds
-// o / (l sc) in fp16 and adds w[G] = l sc, the weight its o enters the merge
-// with; sc is a power of two, 1 unless the largest |o / l| of the row is
-// above kH16Limit.  Since o / l is a convex combination of V rows, the
-// stored values are bounded by the largest |v| of the chunk.
+// o / (l sc) in fp16, then per row a 16-byte record (m, l, w, 0) with
+// w = l sc, the weight its o enters the merge with; sc is a power of two, 1
+// unless the largest |o / l| of the row is above kH16Limit.  Since o / l is
+// a convex combination of V rows, the stored values are bounded by the
+// largest |v| of the chunk.
 //
 // A 16-bit row is stored in groups of eight values, d0 .. d0 + 3 and
 // d0 + 16 .. d0 + 19 for d0 = 32 u + 4 q (q < 4), at group 4 u + q: the
@@ -112,9 +113,9 @@ struct Slot {
             return (uint32_t)(h * D + d) * 4u;
         }
     }
-    __device__ static uint32_t m(int h) { return ML + 4u * (uint32_t)h; }
-    __device__ static uint32_t l(int h) { return ML + 4u * (uint32_t)(G + h); }
-    __device__ static uint32_t w(int h) { return ML + 4u * (uint32_t)(2 * G + h); }
+    __device__ static uint32_t m(int h) { return H16 ? ML + 16u * (uint32_t)h : ML + 4u * (uint32_t)h; }
+    __device__ static uint32_t l(int h) { return H16 ? ML + 16u * (uint32_t)h + 4u : ML + 4u * (uint32_t)(G + h); }
+    __device__ static uint32_t w(int h) { return ML + 16u * (uint32_t)h + 8u; }   // H16 only
 };
 constexpr float kH16Limit = 32768.f;
 
@@ -133,13 +134,16 @@ __device__ __forceinline__ void load_pslot(__amdgpu_buffer_rsrc_t r, uint32_t ba
     using SL = Slot<D, G, H16>;
     if constexpr (H16) {
         o = part_load4h(r, base + SL::o(h, d));
-        w = part_load1(r, base + SL::w(h));
+        const f32x4_t mlw = part_load4(r, base + SL::m(h));
+        m = mlw.x;
+        l = mlw.y;
+        w = mlw.z;
     } else {
         o = part_load4(r, base + SL::o(h, d));
+        m = part_load1(r, base + SL::m(h));
+        l = part_load1(r, base + SL::l(h));
+        w = l;
     }
-    m = part_load1(r, base + SL::m(h));
-    l = part_load1(r, base + SL::l(h));
-    if constexpr (!H16) w = l;
 }
 
 // ---------------------------------------------------------- vector-ALU rows
@@ -840,11 +844,7 @@ __device__ int fused_prompt_item(const AttnArgs &a, int item, char *lds, int *s_
                 __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4_t, h), r,
                                                        slot + SL::o(hh[rb], 32 * u + 4 * quad), 0, kSc1);
             });
-            if (quad == 0) {
-                part_store1(r, slot + SL::m(hh[rb]), S.m[rb]);
-                part_store1(r, slot + SL::l(hh[rb]), l);
-                part_store1(r, slot + SL::w(hh[rb]), l * sc);
-            }
+            if (quad == 0) part_store4(r, slot + SL::m(hh[rb]), f32x4_t{S.m[rb], l, l * sc, 0.f});
         }
     });
     stores_performed();
@@ -909,9 +909,10 @@ __device__ __forceinline__ void gen_merge_in_place(const AttnArgs &a, const Wave
                 if (j < a.n_p) {
                     const uint32_t off = sbase + (uint32_t)j * a.p_slot_bytes;
                     ok[u][j] = __builtin_amdgcn_raw_buffer_load_b128(r, off + SL::o(he[u], de[u]), 0, kSc1);
-                    mk[u][j] = part_load1(r, off + SL::m(he[u]));
-                    lk[u][j] = part_load1(r, off + SL::l(he[u]));
-                    wk[u][j] = part_load1(r, off + SL::w(he[u]));
+                    const f32x4_t mlw = part_load4(r, off + SL::m(he[u]));
+                    mk[u][j] = mlw.x;
+                    lk[u][j] = mlw.y;
+                    wk[u][j] = mlw.z;
                 }
             }
         });

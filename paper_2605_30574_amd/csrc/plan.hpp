@@ -146,11 +146,11 @@ inline int slot_floats(int G, int D) { return (G * D + 2 * G + 63) / 64 * 64; }
 inline bool bf16_path(const splice_shape &sh) { return sh.dtype == SPLICE_BF16; }
 
 // Bytes per prompt slot: an fp32 slot, or for bf16 inputs a 16-bit one
-// (o[G][D] in fp16, then m[G], l[G] and the weights w[G] in fp32, padded to
+// (o[G][D] in fp16, then a 16-byte record (m, l, w, 0) per row, padded to
 // 256 bytes), never larger than an fp32 slot.
 inline int prompt_slot_bytes(const splice_shape &sh) {
     const int G = group_of(sh), D = sh.head_dim;
-    return bf16_path(sh) ? round_up((int64_t)G * D * 2 + 12 * G, 256) : slot_floats(G, D) * 4;
+    return bf16_path(sh) ? round_up((int64_t)G * D * 2 + 16 * G, 256) : slot_floats(G, D) * 4;
 }
 
 // bf16 row groups of one KV head: the rows of unspliced cells and the rows
