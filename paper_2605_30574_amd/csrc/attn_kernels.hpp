@@ -444,9 +444,10 @@ __device__ void prompt_item_valu(const AttnArgs &a, int c, int g, int pk, char *
 // The combine of one (row, four outputs) is fixed: M = the maximum of the
 // slots' m (and 0 with a ZERO term); L starts at the ZERO term
 // n_zero 2^-M (or 0); then slot k = 0, 1, ... adds l_k 2^(m_k - M) to L and
-// o_k 2^(m_k - M) to O with one fused multiply-add per value; out = O / L.
-// Every merge site below follows it, so a result does not depend on which
-// item merged it.
+// o_k 2^(m_k - M) to O with one fused multiply-add per value (a 16-bit
+// prompt slot: its stored o times w_k 2^(m_k - M), the product rounded
+// once); out = O / L.  Every merge site below follows it, so a result does
+// not depend on which item merged it.
 
 __device__ __forceinline__ void stores_performed() {
     __builtin_amdgcn_s_waitcnt(0);   // every outstanding memory operation of this lane is done
