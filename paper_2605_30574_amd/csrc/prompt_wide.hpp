@@ -99,17 +99,15 @@ __device__ __forceinline__ u32x4_t rows_desc(const char *base, int bytes) {
 // inline assembly on purpose: the compiler, which cannot tell the ring's
 // buffers apart, would otherwise wait for every load in flight before each
 // LDS read (s_waitcnt vmcnt(0)) and undo the prefetch; the stream waits on
-// vmcnt itself.  M0 (the LDS base) is saved and restored around the load.
+// vmcnt itself.  M0 holds the LDS base; the statement declares M0 clobbered,
+// so the compiler keeps nothing in it across the load.
 __device__ __forceinline__ void lds_dma16(u32x4_t desc, uint32_t lds_addr, int voff) {
-    uint32_t saved;
     asm volatile(
-        "s_mov_b32 %0, m0\n\t"
-        "s_mov_b32 m0, %1\n\t"
-        "buffer_load_dwordx4 %2, %3, 0 offen lds\n\t"
-        "s_mov_b32 m0, %0"
-        : "=&s"(saved)
+        "s_mov_b32 m0, %0\n\t"
+        "buffer_load_dwordx4 %1, %2, 0 offen lds"
+        :
         : "s"(lds_addr), "v"(voff), "s"(desc)
-        : "memory");
+        : "memory", "m0");
 }
 
 __device__ __forceinline__ uint32_t lds_offset(const char *p) {
