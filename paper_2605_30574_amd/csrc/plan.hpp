@@ -171,17 +171,19 @@ inline int row_groups(const splice_shape &sh, int n_clean, int n_active) {
 inline int prompt_items_per_chunk(const splice_shape &sh, int n_clean) {
     return sh.n_kv_heads * (bf16_path(sh) ? row_groups(sh, n_clean, sh.n_cells) : sh.n_cells);
 }
-inline int prompt_items_bound(const splice_shape &sh) {
+// n_active: the cells the call computes (bf16; a decode step with finished
+// cells has fewer, and then takes more, shorter chunks for its prompt items).
+inline int prompt_items_bound(const splice_shape &sh, int n_active) {
     if (!bf16_path(sh)) return sh.n_kv_heads * sh.n_cells;
-    return sh.n_kv_heads * (ceil_div((int64_t)sh.n_cells * group_of(sh), group_rows(sh.head_dim)) + 1);
+    return sh.n_kv_heads * (ceil_div((int64_t)n_active * group_of(sh), group_rows(sh.head_dim)) + 1);
 }
 
 // bf16: at most this many prompt chunks by default, so that a generated-row
 // item merges every prompt slot in one round of loads.
 constexpr int kWideMaxChunks = 16;
 
-inline int prompt_chunk_target(const splice_shape &sh) {
-    const int per = prompt_items_bound(sh);
+inline int prompt_chunk_target(const splice_shape &sh, int n_active) {
+    const int per = prompt_items_bound(sh, n_active);
     const int want = bf16_path(sh) ? kWideItemsTarget : kPromptItemsTarget;
     const int cap = bf16_path(sh) ? kWideMaxChunks : kMaxChunks;
     const int t = per > 0 ? want / per : 1;
@@ -274,13 +276,13 @@ inline AttnPlan plan_from_geo(const splice_shape &sh, const splice_call &call, c
         p.gen_pairs = 1;
         return p;
     }
-    cut(p.geo.n_prompt, prompt_chunk_target(sh), call.split_keys, &p.n_p, &p.p_len,
+    cut(p.geo.n_prompt, prompt_chunk_target(sh, n_active), call.split_keys, &p.n_p, &p.p_len,
         bf16_path(sh) ? kWideMinChunk : kMinChunk);
     if (bf16_path(sh) && call.split_keys == 0) {
         // chunks of a few tiles spend much of their time starting up and
         // storing partials: take longer ones when the grid stays wide enough
         int n_long, len_long;
-        cut(p.geo.n_prompt, prompt_chunk_target(sh), 0, &n_long, &len_long, kWideLongChunk);
+        cut(p.geo.n_prompt, prompt_chunk_target(sh, n_active), 0, &n_long, &len_long, kWideLongChunk);
         const int64_t groups = (int64_t)sh.n_kv_heads * row_groups(sh, n_clean, n_active);
         if (n_long < p.n_p && n_long * groups >= kWideLongChunkItems) {
             p.n_p = n_long;
@@ -344,10 +346,10 @@ struct WorkspaceLayout {
 // wait ran out, counted since splice_workspace_init.
 constexpr size_t kStatsBytes = 256;
 
-// Statistics, counters [C][Hkv] (int32), then the partial results: the
-// region is sized for one fp32 slot per (cell, KV head, chunk), which also
-// holds a bf16 call's smaller prompt slots followed by its generated-row
-// slots.
+// Statistics, counters [C][Hkv] (int32), then the partial results: one
+// slot per (cell, KV head, chunk) -- for bf16 inputs the 16-bit prompt slots
+// [C][Hkv][n_slots - 1] followed by the fp32 generated-row slots [C][Hkv]
+// (one each), otherwise fp32 slots.
 inline WorkspaceLayout workspace_layout(const splice_shape &sh, int n_slots) {
     WorkspaceLayout w;
     const int64_t pairs = (int64_t)sh.n_cells * sh.n_kv_heads;
@@ -355,7 +357,10 @@ inline WorkspaceLayout workspace_layout(const splice_shape &sh, int n_slots) {
     w.counters_off = kStatsBytes;
     w.counters_bytes = (size_t)round_up(pairs * 4, 256);
     w.part_off = w.counters_off + w.counters_bytes;
-    w.part_bytes = (size_t)pairs * (size_t)n_slots * (size_t)slot_floats(group_of(sh), sh.head_dim) * 4;
+    const size_t f32_slot = (size_t)slot_floats(group_of(sh), sh.head_dim) * 4;
+    w.part_bytes = bf16_path(sh) && n_slots > 0
+                       ? (size_t)pairs * ((size_t)(n_slots - 1) * (size_t)prompt_slot_bytes(sh) + f32_slot)
+                       : (size_t)pairs * (size_t)n_slots * f32_slot;
     w.total = w.part_off + w.part_bytes;
     if (w.total < 256) w.total = 256;
     return w;
@@ -372,7 +377,8 @@ inline int max_default_chunks(int n, int target, int min_chunk = kMinChunk) {
 }
 
 inline int worst_default_slots(const splice_shape &sh) {
-    const int prompt = max_default_chunks(sh.prompt_len, prompt_chunk_target(sh),
+    // bf16: a decode step with one active cell takes the most chunks
+    const int prompt = max_default_chunks(sh.prompt_len, prompt_chunk_target(sh, bf16_path(sh) ? 1 : sh.n_cells),
                                           bf16_path(sh) ? kWideMinChunk : kMinChunk);
     return bf16_path(sh) ? prompt + 1 : prompt + max_default_chunks(sh.gen_capacity, gen_chunk_target(sh));
 }
