@@ -232,15 +232,56 @@ struct AttnPlan {
 };
 
 // bf16 generated-row items: a work group of fused_waves(D) waves serves P
-// consecutive cells of one KV head, NW / P waves each.  Each wave should
-// stream at least two 16-row tiles, so short generated parts pack many
-// cells into a work group and long ones spread one cell over all waves.
-inline int gen_pairs(const splice_shape &sh, int n_gen) {
+// consecutive cells of one KV head, NW / P waves each (P = 1, 2 or 4).
+//
+// With an explicit split_keys the grouping depends on the generated length
+// alone, so a cell's bits do not depend on its batch-mates: each wave
+// streams at least two 16-row tiles.
+inline int gen_pairs_fixed(const splice_shape &sh, int n_gen) {
     const int nw = fused_waves(sh.head_dim);
     const int tiles = ceil_div(n_gen, 16);
     int wpp = nw;
     while (wpp > 1 && tiles < 2 * wpp) wpp /= 2;
     return nw / wpp;
+}
+
+// What one GPU holds of the bf16 kernel at once: its compute units and the
+// work groups resident on each (0 when unknown).
+struct Residency {
+    int n_cu = 0;
+    int per_cu = 0;
+};
+
+// Default grouping.  The generated-row streams run fastest when every work
+// group of the launch is resident from the start (no second round whose last
+// groups stream alone), when the groups spread evenly over the compute units
+// (a unit holding one more group than the others finishes last), and when
+// each wave streams enough rows to hide its first loads.  So P is the
+// smallest grouping whose waves stream at least kGenWaveBytes among those
+// that fit beside the prompt items in one round with at most kGenImbalance
+// times the mean groups per unit; if no wave gets that many bytes, the
+// largest such grouping; if none fits, NW.  prompt_items is a bound that does
+// not depend on the clean/spliced split of the cells, so the grouping (and
+// the bits) of a call do not either.
+constexpr int64_t kGenWaveBytes = 48 << 10;
+constexpr int kGenImbalanceNum = 6, kGenImbalanceDen = 5;   // 1.2
+
+inline int gen_pairs_default(const splice_shape &sh, int n_gen, int n_active, int64_t prompt_items,
+                             const Residency &res) {
+    const int nw = fused_waves(sh.head_dim);
+    if (res.n_cu <= 0 || res.per_cu <= 0) return gen_pairs_fixed(sh, n_gen);
+    const int64_t resident = (int64_t)res.n_cu * res.per_cu;
+    const int64_t row_bytes = 2LL * sh.head_dim * elem_bytes(sh);   // a K row and a V row
+    int long_enough = 0, largest = 0;
+    for (int P = 1; P <= nw; P *= 2) {
+        const int64_t groups = (int64_t)ceil_div(n_active, P) * sh.n_kv_heads;
+        if (prompt_items + groups > resident) continue;
+        const int64_t per_unit = ceil_div(groups, res.n_cu);
+        if (groups > res.n_cu && per_unit * res.n_cu * kGenImbalanceDen > groups * kGenImbalanceNum) continue;
+        largest = P;
+        if (!long_enough && (int64_t)n_gen * row_bytes * P >= kGenWaveBytes * nw) long_enough = P;
+    }
+    return long_enough ? long_enough : (largest ? largest : nw);
 }
 
 // Validation of a decode step's per-cell steps (host int32 [C]): each is
@@ -264,7 +305,7 @@ inline int count_clean(const splice_shape &sh, const splice_call &call, const in
 // different steps: the widest visible prompt and the longest generated part)
 // over n_active cells, n_clean of them unspliced.
 inline AttnPlan plan_from_geo(const splice_shape &sh, const splice_call &call, const Geometry &geo, int n_clean,
-                              int n_active) {
+                              int n_active, const Residency &res = Residency()) {
     AttnPlan p;
     p.geo = geo;
     p.cellwise = !bf16_path(sh) && call.split_keys == 0 && p.geo.n_prompt <= kCellwiseMaxPrompt;
@@ -306,7 +347,15 @@ inline AttnPlan plan_from_geo(const splice_shape &sh, const splice_call &call, c
         p.n_prompt_items = prompt_items_per_chunk(sh, n_clean) * p.n_p;
     }
     if (bf16_path(sh)) {
-        p.gen_pairs = gen_pairs(sh, p.geo.n_gen);
+        // the prompt items of the call's grid with one more row group per
+        // KV head than an unsplit one (the most any split of the cells gives)
+        const int64_t prompt_bound =
+            p.n_p > 0 ? (int64_t)kXcds *
+                            (ceil_div((int64_t)n_active * group_of(sh), group_rows(sh.head_dim)) + 1) *
+                            ceil_div((int64_t)sh.n_kv_heads * p.n_p, kXcds)
+                      : 0;
+        p.gen_pairs = call.split_keys > 0 ? gen_pairs_fixed(sh, p.geo.n_gen)
+                                          : gen_pairs_default(sh, p.geo.n_gen, n_active, prompt_bound, res);
         p.n_gen_items = ceil_div(n_active, p.gen_pairs) * sh.n_kv_heads;   // active cells only
     } else {
         p.gen_pairs = 1;

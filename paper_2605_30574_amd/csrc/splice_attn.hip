@@ -129,6 +129,38 @@ void fill_mask(const splice_shape &sh, const splice_call &call, const int32_t *c
         if (splice::cell_spliced(cell_LW, c, call.layer, call.step)) mask[c >> 5] |= 1u << (c & 31);
 }
 
+// Compute units of the current device and work groups of `kernel` (at
+// `threads` threads) resident on each, asked of HIP once per device and
+// kernel; zeros when HIP cannot tell, and the planner then groups the
+// generated rows by their length alone.
+splice::Residency residency(const void *kernel, int threads) {
+    struct Entry {
+        int dev;
+        const void *kernel;
+        splice::Residency res;
+    };
+    static std::mutex mu;
+    static Entry cache[64];
+    static int n_cache = 0;
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess) return splice::Residency();
+    std::lock_guard<std::mutex> lock(mu);
+    for (int i = 0; i < n_cache; ++i)
+        if (cache[i].dev == dev && cache[i].kernel == kernel) return cache[i].res;
+    splice::Residency res;
+    int n_cu = 0, per_cu = 0;
+    if (hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess &&
+        hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kernel, threads, 0) == hipSuccess && n_cu > 0 &&
+        per_cu > 0) {
+        res.n_cu = n_cu;
+        res.per_cu = per_cu;
+    } else {
+        (void)hipGetLastError();   // the call itself has not failed: clear what the queries left
+    }
+    if (n_cache < 64) cache[n_cache++] = Entry{dev, kernel, res};
+    return res;
+}
+
 int32_t launch_status() {
     const hipError_t err = hipGetLastError();
     return err == hipSuccess ? SPLICE_OK : SPLICE_EHIP;
@@ -326,15 +358,18 @@ int32_t decode_attn_impl(const splice_shape *shape, const splice_call *call, con
         else
             ++n_clean;
     }
-    const splice::AttnPlan plan = splice::plan_from_geo(sh, hi_call, geo, n_clean, n_active);
+    const int G = splice::group_of(sh);
+    const AttnKernels kern = pick_attn(sh.head_dim, G, sh.dtype);
+    if (!kern.items) return SPLICE_EUNSUPPORTED;
+    const int threads = splice::bf16_path(sh) ? 64 * splice::fused_waves(sh.head_dim) : kThreads;
+
+    const splice::AttnPlan plan = splice::plan_from_geo(
+        sh, hi_call, geo, n_clean, n_active,
+        splice::bf16_path(sh) ? residency((const void *)kern.items, threads) : splice::Residency());
     if (plan.n_slots > splice::kMaxSlots) return SPLICE_EUNSUPPORTED;
     const splice::WorkspaceLayout wl = splice::workspace_layout(sh, plan.n_slots);
     if (!workspace || !splice::aligned(workspace, 256)) return SPLICE_EWORKSPACE;
     if (workspace_bytes < wl.total) return SPLICE_EWORKSPACE;
-
-    const int G = splice::group_of(sh);
-    const AttnKernels kern = pick_attn(sh.head_dim, G, sh.dtype);
-    if (!kern.items) return SPLICE_EUNSUPPORTED;
 
     AttnArgs a;
     a.q = (const char *)q;
@@ -417,7 +452,6 @@ int32_t decode_attn_impl(const splice_shape *shape, const splice_call *call, con
     }
     const int64_t items = (int64_t)plan.n_prompt_items + plan.n_gen_items;
     if (items > INT32_MAX) return SPLICE_EUNSUPPORTED;
-    const int threads = splice::bf16_path(sh) ? 64 * splice::fused_waves(sh.head_dim) : kThreads;
     hipLaunchKernelGGL(kern.items, dim3((unsigned)items), dim3((unsigned)threads), 0, (hipStream_t)stream, a);
     return launch_status();
 }
