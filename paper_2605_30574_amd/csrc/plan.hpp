@@ -260,14 +260,20 @@ struct Residency {
 // smallest grouping whose waves stream at least kGenWaveBytes among those
 // that fit beside the prompt items in one round with at most kGenImbalance
 // times the mean groups per unit; if no wave gets that many bytes, the
-// largest such grouping; if none fits, NW.  prompt_items is a bound that does
-// not depend on the clean/spliced split of the cells, so the grouping (and
-// the bits) of a call do not either.
+// largest such grouping; if none fits, NW.  When the cells stream different
+// numbers of rows (a decode step with cells at their own steps; n_gen is the
+// longest, and `same_rows` is false), rounds and balance matter less: the
+// longest streams are dispatched first, so the groups that wait are the
+// shortest, and the groups differ in length anyway; what sets the pass is
+// the longest stream, so P is the smallest grouping whose waves stream at
+// least kGenWaveBytes of it.  prompt_items is a bound that does not depend on
+// the clean/spliced split of the cells, so the grouping (and the bits) of a
+// call do not either.
 constexpr int64_t kGenWaveBytes = 48 << 10;
 constexpr int kGenImbalanceNum = 6, kGenImbalanceDen = 5;   // 1.2
 
 inline int gen_pairs_default(const splice_shape &sh, int n_gen, int n_active, int64_t prompt_items,
-                             const Residency &res) {
+                             const Residency &res, bool same_rows) {
     const int nw = fused_waves(sh.head_dim);
     if (res.n_cu <= 0 || res.per_cu <= 0) return gen_pairs_fixed(sh, n_gen);
     const int64_t resident = (int64_t)res.n_cu * res.per_cu;
@@ -275,9 +281,11 @@ inline int gen_pairs_default(const splice_shape &sh, int n_gen, int n_active, in
     int long_enough = 0, largest = 0;
     for (int P = 1; P <= nw; P *= 2) {
         const int64_t groups = (int64_t)ceil_div(n_active, P) * sh.n_kv_heads;
-        if (prompt_items + groups > resident) continue;
-        const int64_t per_unit = ceil_div(groups, res.n_cu);
-        if (groups > res.n_cu && per_unit * res.n_cu * kGenImbalanceDen > groups * kGenImbalanceNum) continue;
+        if (same_rows) {
+            if (prompt_items + groups > resident) continue;
+            const int64_t per_unit = ceil_div(groups, res.n_cu);
+            if (groups > res.n_cu && per_unit * res.n_cu * kGenImbalanceDen > groups * kGenImbalanceNum) continue;
+        }
         largest = P;
         if (!long_enough && (int64_t)n_gen * row_bytes * P >= kGenWaveBytes * nw) long_enough = P;
     }
@@ -305,7 +313,7 @@ inline int count_clean(const splice_shape &sh, const splice_call &call, const in
 // different steps: the widest visible prompt and the longest generated part)
 // over n_active cells, n_clean of them unspliced.
 inline AttnPlan plan_from_geo(const splice_shape &sh, const splice_call &call, const Geometry &geo, int n_clean,
-                              int n_active, const Residency &res = Residency()) {
+                              int n_active, const Residency &res = Residency(), bool same_rows = true) {
     AttnPlan p;
     p.geo = geo;
     p.cellwise = !bf16_path(sh) && call.split_keys == 0 && p.geo.n_prompt <= kCellwiseMaxPrompt;
@@ -355,7 +363,8 @@ inline AttnPlan plan_from_geo(const splice_shape &sh, const splice_call &call, c
                             ceil_div((int64_t)sh.n_kv_heads * p.n_p, kXcds)
                       : 0;
         p.gen_pairs = call.split_keys > 0 ? gen_pairs_fixed(sh, p.geo.n_gen)
-                                          : gen_pairs_default(sh, p.geo.n_gen, n_active, prompt_bound, res);
+                                          : gen_pairs_default(sh, p.geo.n_gen, n_active, prompt_bound, res,
+                                                              same_rows);
         p.n_gen_items = ceil_div(n_active, p.gen_pairs) * sh.n_kv_heads;   // active cells only
     } else {
         p.gen_pairs = 1;

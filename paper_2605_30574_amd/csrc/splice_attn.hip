@@ -365,7 +365,8 @@ int32_t decode_attn_impl(const splice_shape *shape, const splice_call *call, con
 
     const splice::AttnPlan plan = splice::plan_from_geo(
         sh, hi_call, geo, n_clean, n_active,
-        splice::bf16_path(sh) ? residency((const void *)kern.items, threads) : splice::Residency());
+        splice::bf16_path(sh) ? residency((const void *)kern.items, threads) : splice::Residency(),
+        g_lo.n_gen == g_hi.n_gen);
     if (plan.n_slots > splice::kMaxSlots) return SPLICE_EUNSUPPORTED;
     const splice::WorkspaceLayout wl = splice::workspace_layout(sh, plan.n_slots);
     if (!workspace || !splice::aligned(workspace, 256)) return SPLICE_EWORKSPACE;
