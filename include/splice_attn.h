@@ -136,9 +136,10 @@ SPLICE_API int32_t splice_kv_build(const splice_shape *shape, const splice_call 
                         void *stream);
 
 /*
- * Workspace bytes splice_decode_attn needs for `call`.  With call == NULL:
- * enough for every call on `shape` with split_keys == 0 (any layer, step,
- * window).  Negative splice_status on bad input.
+ * Workspace bytes splice_decode_attn and splice_decode_forked need for
+ * `call` (for a forked sweep, whichever cells have diverged).  With
+ * call == NULL: enough for every call on `shape` with split_keys == 0 (any
+ * layer, step, window, cells computed).  Negative splice_status on bad input.
  */
 SPLICE_API int64_t splice_decode_attn_workspace_bytes(const splice_shape *shape, const splice_call *call);
 

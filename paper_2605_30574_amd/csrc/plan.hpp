@@ -178,6 +178,14 @@ inline int prompt_items_bound(const splice_shape &sh, int n_active) {
     return sh.n_kv_heads * (ceil_div((int64_t)n_active * group_of(sh), group_rows(sh.head_dim)) + 1);
 }
 
+// Cost model of the sparse prompt grid (plan_from_geo), measured on MI355X:
+// a prompt work group alone on its compute unit (beside one generated-row
+// work group) takes about 0.44 us per 32-key tile at D = 128 (16 KiB of K
+// and V), i.e. ~27.5 ns per KiB of its tiles, and the generated rows of a
+// call stream at about 6.8 TB/s.
+constexpr double kPromptChainNsPerKiB = 27.5;
+constexpr double kGenBytesPerNs = 6800.0;
+
 // bf16: at most this many prompt chunks by default, so that a generated-row
 // item merges every prompt slot in one round of loads.
 constexpr int kWideMaxChunks = 16;
@@ -332,10 +340,28 @@ inline AttnPlan plan_from_geo(const splice_shape &sh, const splice_call &call, c
         // storing partials: take longer ones when the grid stays wide enough
         int n_long, len_long;
         cut(p.geo.n_prompt, prompt_chunk_target(sh, n_active), 0, &n_long, &len_long, kWideLongChunk);
-        const int64_t groups = (int64_t)sh.n_kv_heads * row_groups(sh, n_clean, n_active);
+        const int64_t groups = prompt_items_bound(sh, n_active);
         if (n_long < p.n_p && n_long * groups >= kWideLongChunkItems) {
             p.n_p = n_long;
             p.p_len = len_long;
+        }
+        // a long generated part: fewer, longer chunks, at most one prompt
+        // work group per compute unit, when their chains still end before
+        // the generated rows are streamed
+        if (same_rows && res.n_cu > 0 && groups > 0) {
+            const int n_sparse = (int)(res.n_cu / groups);
+            if (n_sparse >= 1 && n_sparse < p.n_p) {
+                int k, len;
+                cut(p.geo.n_prompt, n_sparse, 0, &k, &len, kWideMinChunk);
+                const double prompt_ns = (double)ceil_div(len, 32) * 64.0 * sh.head_dim * elem_bytes(sh) / 1024.0 *
+                                         kPromptChainNsPerKiB;
+                const double gen_ns = (double)n_active * sh.n_kv_heads * p.geo.n_gen * 2.0 * sh.head_dim *
+                                      elem_bytes(sh) / kGenBytesPerNs;
+                if (gen_ns >= prompt_ns) {
+                    p.n_p = k;
+                    p.p_len = len;
+                }
+            }
         }
     }
     if (bf16_path(sh)) {
@@ -386,10 +412,6 @@ inline bool gen_v_nontemporal(const splice_shape &sh, int n_gen) {
     const int64_t per_cache = (int64_t)sh.prompt_len * sh.n_kv_heads * sh.head_dim * elem_bytes(sh) * 2;
     const int64_t bytes = per_cache * (sh.donor_kind == SPLICE_DONOR_BUFFER ? 2 : 1);
     return bytes > kGenNtPromptBytes || n_gen >= kGenNtRows;
-}
-
-inline AttnPlan plan_attn(const splice_shape &sh, const splice_call &call, int n_clean) {
-    return plan_from_geo(sh, call, geometry(sh, call), n_clean, sh.n_cells);
 }
 
 struct WorkspaceLayout {

@@ -161,6 +161,33 @@ splice::Residency residency(const void *kernel, int threads) {
     return res;
 }
 
+// Workspace bytes of `call` on `shape` (call == NULL: every default-split
+// call).  With every_count the bytes cover any number of computed cells:
+// a forked sweep plans over its diverged cells only, and by default fewer
+// computed cells take more prompt chunks (with an explicit split_keys the
+// chunks do not depend on them); without it, a call that computes every cell.
+int64_t attn_workspace_bytes(const splice_shape *shape, const splice_call *call, bool every_count) {
+    int32_t rc = splice::validate_shape(shape);
+    if (rc != SPLICE_OK) return rc;
+    int n_slots;
+    if (call) {
+        rc = splice::validate_call(*shape, call);
+        if (rc != SPLICE_OK) return rc;
+        const splice::Geometry geo = splice::geometry(*shape, *call);
+        const int n_hi = shape->n_cells > 0 ? shape->n_cells : 1;
+        const int n_lo = every_count && call->split_keys == 0 ? 1 : n_hi;
+        n_slots = 0;
+        for (int n = n_lo; n <= n_hi; ++n) {   // the slots do not depend on the cell split
+            const int k = splice::plan_from_geo(*shape, *call, geo, 0, n).n_slots;
+            n_slots = k > n_slots ? k : n_slots;
+        }
+        if (n_slots > splice::kMaxSlots) return SPLICE_EUNSUPPORTED;
+    } else {
+        n_slots = splice::worst_default_slots(*shape);
+    }
+    return (int64_t)splice::workspace_layout(*shape, n_slots).total;
+}
+
 int32_t launch_status() {
     const hipError_t err = hipGetLastError();
     return err == hipSuccess ? SPLICE_OK : SPLICE_EHIP;
@@ -237,18 +264,7 @@ int32_t splice_kv_build(const splice_shape *shape, const splice_call *call, cons
 }
 
 int64_t splice_decode_attn_workspace_bytes(const splice_shape *shape, const splice_call *call) {
-    int32_t rc = splice::validate_shape(shape);
-    if (rc != SPLICE_OK) return rc;
-    int n_slots;
-    if (call) {
-        rc = splice::validate_call(*shape, call);
-        if (rc != SPLICE_OK) return rc;
-        n_slots = splice::plan_attn(*shape, *call, 0).n_slots;   // slots do not depend on the cell split
-        if (n_slots > splice::kMaxSlots) return SPLICE_EUNSUPPORTED;
-    } else {
-        n_slots = splice::worst_default_slots(*shape);
-    }
-    return (int64_t)splice::workspace_layout(*shape, n_slots).total;
+    return attn_workspace_bytes(shape, call, true);
 }
 
 int32_t splice_workspace_init(void *workspace, size_t workspace_bytes, void *stream) {
@@ -513,7 +529,7 @@ int32_t splice_decode_attn_noalloc(const splice_shape *shape, const splice_call 
                                    void *stream) {
     // validation and the size check come first: a call that does not fit is
     // rejected before any device work
-    const int64_t need = splice_decode_attn_workspace_bytes(shape, call);
+    const int64_t need = attn_workspace_bytes(shape, call, false);   // every cell is computed
     if (need < 0) return (int32_t)need;
     if (need > (int64_t)SPLICE_NOALLOC_WORKSPACE_BYTES) return SPLICE_EWORKSPACE;
     void *ws = nullptr;
