@@ -154,6 +154,37 @@ def test_workspace_bound_covers_every_call():
                 assert need <= worst, (C, Hkv, Tp, cap, step, window)
 
 
+def _bf16_slots(sh, nbytes):
+    """Partial-result slots per (cell, KV head) that a bf16 workspace of nbytes
+    holds: statistics (256 bytes), int32 counters per pair rounded up to 256
+    bytes, then per pair 16-bit prompt slots and one fp32 generated-row slot."""
+    G, D = sh.n_q_heads // sh.n_kv_heads, sh.head_dim
+    pairs = sh.n_cells * sh.n_kv_heads
+    up = lambda x, m: (x + m - 1) // m * m
+    pslot, gslot = up(G * D * 2 + 16 * G, 256), up(G * D + 2 * G, 64) * 4
+    part = nbytes - 256 - up(pairs * 4, 256)
+    assert (part - pairs * gslot) % (pairs * pslot) == 0
+    return 1 + (part - pairs * gslot) // (pairs * pslot)
+
+
+def test_call_workspace_covers_fewer_computed_cells():
+    """A forked sweep computes its diverged cells only, and fewer computed
+    cells take more prompt chunks by default: the bytes for a call on C
+    cells must hold the slots the same call needs with any n <= C computed
+    (what the call needs on a shape of n cells)."""
+    for (C, Tp, window) in ((25, 1024, 0), (128, 8192, 0), (48, 4096, 1024)):
+        for step in (0, 64, 255):
+            call = sp.make_call(0, step, window, 0.125)
+            sh = _shape(dtype="bf16", n_cells=C, n_q_heads=32, n_kv_heads=8, head_dim=128, prompt_len=Tp,
+                        span=(8, Tp - 8), gen_capacity=256, n_layers=4)
+            have = _bf16_slots(sh, sp.splice_decode_attn_workspace_bytes(sh, call))
+            for n in (1, 2, 4, 9, C // 2, C):
+                shn = _shape(dtype="bf16", n_cells=n, n_q_heads=32, n_kv_heads=8, head_dim=128, prompt_len=Tp,
+                             span=(8, Tp - 8), gen_capacity=256, n_layers=4)
+                need = _bf16_slots(shn, sp.splice_decode_attn_workspace_bytes(shn, call))
+                assert need <= have, (C, Tp, window, step, n, need, have)
+
+
 def test_decode_step_validation_before_device_access():
     lib = sp.load_library()
     sh = _shape(dtype="bf16")
