@@ -516,9 +516,15 @@ __device__ __forceinline__ int zero_slots(const AttnArgs &a, int c) {
 
 __device__ __forceinline__ bool has_zero_term(const AttnArgs &a, int c) { return zero_slots(a, c) > 0; }
 
-// Output row (cell c, q head hq): four outputs at d, and lse.  Under a forked
-// sweep the trunk's rows are also the rows of every cell that has not yet
-// diverged from it.
+// Set (in LDS) when this work group has written rows of a forked sweep's
+// trunk: the work group then copies them to the cells that have not yet
+// diverged from it (dormant_copy).
+__device__ __forceinline__ int &trunk_written() {
+    __shared__ int flag;
+    return flag;
+}
+
+// Output row (cell c, q head hq): four outputs at d, and lse.
 __device__ __forceinline__ void write_row(const AttnArgs &a, int c, int hq, int d, int D, float M, float L,
                                           f32x4_t O) {
     const f32x4_t o = O * (1.f / L);
@@ -526,12 +532,42 @@ __device__ __forceinline__ void write_row(const AttnArgs &a, int c, int hq, int 
     const size_t row = (size_t)c * a.Hq + hq;
     *reinterpret_cast<f32x4_t *>(a.out + row * D + d) = o;
     if (d == 0) a.lse[row] = lse;
-    if (c == a.trunk) {
-        for (int i = 0; i < a.n_dormant; ++i) {
-            const size_t r2 = (size_t)a.order[a.n_active + i] * a.Hq + hq;
-            *reinterpret_cast<f32x4_t *>(a.out + r2 * D + d) = o;
-            if (d == 0) a.lse[r2] = lse;
-        }
+    if (c == a.trunk) trunk_written() = 1;
+}
+
+// Under a forked sweep the trunk's rows are also the rows of every cell that
+// has not yet diverged from it.  The work group that wrote the trunk's rows
+// of KV head g copies them, all its threads at once: it stages the dormant
+// cells' indices in LDS (buf) and reads the trunk's rows once, each thread
+// keeping its units in registers, then only stores.  The rows were written
+// by this work group, so a work-group fence and barrier make them readable
+// (they are in this compute unit's L2, and its L1 holds no older copy: out
+// is only ever written).
+template <int D, int G, int NT>
+__device__ void dormant_copy(const AttnArgs &a, int g, char *buf) {
+    constexpr int U = G * D / 4;                     // 16-byte units of one cell's rows of KV head g
+    constexpr int GROUPS = U <= NT ? NT / U : 1;     // thread groups taking every GROUPS-th cell
+    constexpr int UPT = U <= NT ? 1 : U / NT;        // units per thread
+    static_assert(U <= NT ? NT % U == 0 : U % NT == 0, "whole units per thread");
+    __threadfence_block();
+    __syncthreads();
+    int *cells = reinterpret_cast<int *>(buf);
+    for (int i = threadIdx.x; i < a.n_dormant; i += NT) cells[i] = a.order[a.n_active + i];
+    const int grp = U <= NT ? (int)threadIdx.x / U : 0;
+    const int u0 = U <= NT ? (int)threadIdx.x % U : (int)threadIdx.x;
+    const size_t src = ((size_t)a.trunk * a.Hq + (size_t)g * G) * D;
+    f32x4_t v[UPT];
+    static_for<0, UPT>([&](auto j) {
+        v[j] = *reinterpret_cast<const f32x4_t *>(a.out + src + 4 * (u0 + (int)j * NT));
+    });
+    const float l = u0 < G ? a.lse[(size_t)a.trunk * a.Hq + (size_t)g * G + u0] : 0.f;
+    __syncthreads();
+    for (int i = grp; i < a.n_dormant; i += GROUPS) {
+        const size_t row = (size_t)cells[i] * a.Hq + (size_t)g * G;
+        static_for<0, UPT>([&](auto j) {
+            *reinterpret_cast<f32x4_t *>(a.out + row * D + 4 * (u0 + (int)j * NT)) = v[j];
+        });
+        if (u0 < G) a.lse[row + u0] = l;
     }
 }
 
@@ -1124,7 +1160,10 @@ void fused_kernel(AttnArgs a) {
     constexpr int MAXM = fused_max_merge<D, G>();
     __shared__ int s_list[1 + MAXM];   // [0] count, [1..] cells to merge
     static_assert(MAXM <= Fused<D>::NT, "one thread per cell of a row group");
-    if (threadIdx.x == 0) s_list[0] = 0;
+    if (threadIdx.x == 0) {
+        s_list[0] = 0;
+        trunk_written() = 0;
+    }
     __syncthreads();
     const int g = (int)blockIdx.x < a.n_prompt_items
                       ? fused_prompt_item<D, G>(a, blockIdx.x, lds, s_list)
@@ -1135,6 +1174,10 @@ void fused_kernel(AttnArgs a) {
     for (int i = 0; i < n; i += per) {
         combine_cells<D, G, Fused<D>::NT, true>(a, s_list + 1 + i, min(per, n - i), g, lds);
         __syncthreads();
+    }
+    if (a.trunk >= 0 && a.n_dormant > 0) {   // uniform: a forked sweep
+        __syncthreads();
+        if (trunk_written()) dormant_copy<D, G, Fused<D>::NT>(a, g, lds);
     }
 }
 
