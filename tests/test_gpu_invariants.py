@@ -2,6 +2,8 @@
 donor == clean and onsets past the step are bit-identical to unspliced, a
 cell's result does not depend on its batch-mates, repeat calls are
 bit-identical, and the split of the key list changes only rounding."""
+import sys
+
 import numpy as np
 import pytest
 import torch
@@ -208,6 +210,57 @@ def test_graph_replay_matches_eager():
             assert torch.equal(outs[k], ref[k][0]) and torch.equal(lses[k], ref[k][1]), (rep, k)
         issue()                                  # eager work between replays
         torch.cuda.synchronize()
+
+
+_FIRST_CALL_IN_GRAPH = r"""
+import sys
+import torch
+import paper_2605_30574_amd as sp
+import workloads
+w = workloads.get("qwen3-4b")
+layer, step = 17, 300
+lw = workloads.cell_lw(w)
+b = workloads.make_layer(w, layer, device="cuda")
+q = workloads.make_q(w, layer, step, device="cuda")
+shape = sp.make_shape(w.n_cells, w.n_layers, w.n_q_heads, w.n_kv_heads, w.head_dim, w.prompt_len, w.span,
+                      w.n_steps, w.donor == workloads.DONOR_ZERO, w.dtype)
+call = sp.make_call(layer, step, w.window(layer), w.scale)
+ws = sp.new_workspace(shape)
+out = [torch.full((w.n_cells, w.n_q_heads, w.head_dim), float("nan"), device="cuda") for _ in range(2)]
+lse = [torch.full((w.n_cells, w.n_q_heads), float("nan"), device="cuda") for _ in range(2)]
+def run(i):
+    sp.splice_decode_attn(shape, call, lw, q, b["clean_k"], b["clean_v"], b["donor_k"], b["donor_v"],
+                          b["gen_k"], b["gen_v"], out[i], lse[i], ws)
+torch.cuda.synchronize()
+stream = torch.cuda.Stream()
+stream.wait_stream(torch.cuda.current_stream())
+g = torch.cuda.CUDAGraph()
+with torch.cuda.graph(g, stream=stream):   # the process's first attention call
+    run(0)
+g.replay()
+torch.cuda.synchronize()
+run(1)
+torch.cuda.synchronize()
+ok = torch.equal(out[0], out[1]) and torch.equal(lse[0], lse[1]) and bool(torch.isfinite(out[0]).all())
+print("first-call-in-graph", "ok" if ok else "MISMATCH", flush=True)
+sys.exit(0 if ok else 1)
+"""
+
+
+def test_first_call_inside_graph_capture():
+    """The library asks HIP for the device's compute units and the kernel's
+    residency on its first call on a device; when that first call is being
+    captured into a graph, the queries must not break the capture, and the
+    replay must give the eager call's bits.  Run in a fresh process, whose
+    first attention call is the captured one."""
+    import os
+    import subprocess
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    gc.announce("first call inside graph capture (subprocess)")
+    env = dict(os.environ, PYTHONPATH=root + os.pathsep + os.environ.get("PYTHONPATH", ""))
+    res = subprocess.run([sys.executable, "-c", _FIRST_CALL_IN_GRAPH], cwd=root, env=env, capture_output=True,
+                         text=True, timeout=240)
+    assert res.returncode == 0 and "first-call-in-graph ok" in res.stdout, (res.stdout[-2000:], res.stderr[-2000:])
 
 
 def test_workspace_reuse_gives_fresh_workspace_bits():
