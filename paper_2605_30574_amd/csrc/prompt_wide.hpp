@@ -155,8 +155,8 @@ __device__ __forceinline__ void direct_issue(const TileRef &t, uint32_t base, co
     });
 }
 
-// One tile from LDS for this wave's RB row blocks (the arithmetic of
-// wide_compute; only the operand reads differ).
+// One tile from LDS for this wave's RB row blocks: q.k, the online softmax
+// of each row, p.v.
 template <int D, int RB>
 __device__ __forceinline__ void direct_compute(const char *buf, int n_valid, int key0, bool row_lo,
                                                const int (&lo)[RB],
