@@ -178,6 +178,10 @@ inline int prompt_items_bound(const splice_shape &sh, int n_active) {
     return sh.n_kv_heads * (ceil_div((int64_t)n_active * group_of(sh), group_rows(sh.head_dim)) + 1);
 }
 
+// Keys per prompt tile of the bf16 kernel (one K and one V tile per step of
+// a prompt work group's chain).
+constexpr int kPromptTileKeys = 32;
+
 // Cost model of the sparse prompt grid (plan_from_geo), measured on MI355X:
 // a prompt work group alone on its compute unit (beside one generated-row
 // work group) takes about 0.44 us per 32-key tile at D = 128 (16 KiB of K
@@ -266,8 +270,9 @@ struct Residency {
 // (a unit holding one more group than the others finishes last), and when
 // each wave streams enough rows to hide its first loads.  So P is the
 // smallest grouping whose waves stream at least kGenWaveBytes among those
-// that fit beside the prompt items in one round with at most kGenImbalance
-// times the mean groups per unit; if no wave gets that many bytes, the
+// that fit beside the prompt items in one round with at most 1.2 times
+// the mean groups per unit (kGenImbalanceNum / kGenImbalanceDen); if no
+// wave gets that many bytes, the
 // largest such grouping; if none fits, NW.  When the cells stream different
 // numbers of rows (a decode step with cells at their own steps; n_gen is the
 // longest, and `same_rows` is false), rounds and balance matter less: the
@@ -353,8 +358,8 @@ inline AttnPlan plan_from_geo(const splice_shape &sh, const splice_call &call, c
             if (n_sparse >= 1 && n_sparse < p.n_p) {
                 int k, len;
                 cut(p.geo.n_prompt, n_sparse, 0, &k, &len, kWideMinChunk);
-                const double prompt_ns = (double)ceil_div(len, 32) * 64.0 * sh.head_dim * elem_bytes(sh) / 1024.0 *
-                                         kPromptChainNsPerKiB;
+                const double tile_kib = 2.0 * kPromptTileKeys * sh.head_dim * elem_bytes(sh) / 1024.0;   // K and V
+                const double prompt_ns = (double)ceil_div(len, kPromptTileKeys) * tile_kib * kPromptChainNsPerKiB;
                 const double gen_ns = (double)n_active * sh.n_kv_heads * p.geo.n_gen * 2.0 * sh.head_dim *
                                       elem_bytes(sh) / kGenBytesPerNs;
                 if (gen_ns >= prompt_ns) {

@@ -44,7 +44,7 @@ struct WideState {
 // flight; one barrier per tile.
 template <int D>
 struct Direct {
-    static constexpr int TK = 32;                                  // keys per tile
+    static constexpr int TK = splice::kPromptTileKeys;             // keys per tile
     static constexpr int ROW = D * 2;                              // bytes per K or V row
     static constexpr int CH = ROW / 16;                            // 16-byte chunks per row
     static constexpr int TILE = TK * ROW;                          // K (or V) tile bytes
