@@ -36,6 +36,11 @@ Reported (one JSON line):
               (the workload's attention shape, its model's hidden sizes):
               ms per pass of all N layers plus the argmax, at the bucket
               steps, cell-steps/s, and the attention's share of a pass;
+  read_ceiling  the rate of a plain stream read of a 4 GiB device buffer
+              (libsplice_calib.so: contiguous parts per work group, 16-byte
+              non-temporal loads; the best of three grid sizes, HIP events
+              over ten launches each), measured in the same process after
+              the timed region, and the sweep's GB/s as a share of it;
   decode_step  splice_decode_step passes (each cell at its own step, the
               current token's K/V appended, finished cells skipped) over two
               seeded step mixes -- 1/8 and 1/2 of the cells finished --
@@ -400,6 +405,39 @@ def sweep_summary(w, r, K: int):
                        "span": list(w.span), "decode_steps": w.n_steps, "donor": w.donor}}
 
 
+# ------------------------------------------------------------ read ceiling
+
+def read_ceiling(dev, gib: int = 4, reps: int = 10) -> dict:
+    """The rate of libsplice_calib.so's stream read over a `gib` GiB device
+    buffer (16 times the last-level cache, so every launch reads from HBM):
+    HIP events over `reps` launches after one untimed launch, for 1024, 2048
+    and 4096 work groups; the best of the three."""
+    import torch
+
+    from paper_2605_30574_amd import calib
+    n = gib << 30
+    buf = torch.empty(n, dtype=torch.uint8, device=dev)
+    sink = torch.empty(calib.MAX_BLOCKS, dtype=torch.int32, device=dev)
+    stream = torch.cuda.Stream(device=dev)
+    stream.wait_stream(torch.cuda.current_stream(dev))
+    rates = {}
+    for blocks in (1024, 2048, 4096):
+        calib.stream_read(buf, sink, blocks, stream)
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(reps):
+            calib.stream_read(buf, sink, blocks, stream)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        rates[blocks] = n * reps / (e0.elapsed_time(e1) / 1e3) / 1e9
+    del buf, sink
+    torch.cuda.empty_cache()
+    best = max(rates, key=rates.get)
+    return {"GB/s": round(rates[best], 1), "blocks": best, "bytes": n, "launches": reps,
+            "kernel": "stream_read_kernel", "per_blocks": {str(b): round(r, 1) for b, r in rates.items()}}
+
+
 # ------------------------------------------------------------------ main
 
 def main():
@@ -668,6 +706,9 @@ def main():
     del sw, layers, qs, ws, out, lse, run
     torch.cuda.synchronize()
     torch.cuda.empty_cache()
+    ceiling = read_ceiling(dev)
+    log(f"stream-read ceiling: {ceiling['GB/s']} GB/s ({ceiling['blocks']} work groups); "
+        f"the sweep reaches {100 * gbs / ceiling['GB/s']:.1f}% of it")
     also = {}
     for name in [n for n in args.also.split(",") if n and n != w.name]:
         w2 = workloads.get(name)
@@ -692,6 +733,8 @@ def main():
         "pct_of_hbm_peak": round(100 * gbs / HBM_PEAK_GBS, 2),
         "cell_steps_per_s": round(C * K / sec, 1),
         "merges_handed_over": handovers,
+        "read_ceiling": ceiling,
+        "pct_of_read_ceiling": round(100 * gbs / ceiling["GB/s"], 2),
         "config": {"workload": w.name, "layers": N, "cells": C, "q_heads": w.n_q_heads,
                    "kv_heads": w.n_kv_heads, "head_dim": w.head_dim, "prompt_len": w.prompt_len,
                    "span": list(w.span), "decode_steps": S, "donor": w.donor,

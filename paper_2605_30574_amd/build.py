@@ -1,4 +1,6 @@
-"""Build the gfx950 splice library in-tree: paper_2605_30574_amd/libsplice_attn.so.
+"""Build the gfx950 libraries in-tree: paper_2605_30574_amd/libsplice_attn.so
+(the spliced decode attention) and paper_2605_30574_amd/libsplice_calib.so (a
+plain stream-read kernel, the measured read ceiling).
 
     python -m paper_2605_30574_amd.build
 
@@ -21,6 +23,8 @@ INCLUDE = os.path.join(ROOT, "include")
 CSRC = os.path.join(PKG, "csrc")
 OBJDIR = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libsplice_attn.so")
+CALIB_SRC = os.path.join(PKG, "calib", "stream_read.hip")
+CALIB_LIB = os.path.join(PKG, "libsplice_calib.so")
 ARCH = "gfx950"
 
 COMPILE_FLAGS = [
@@ -81,5 +85,16 @@ def build(out: str = LIB, extra=(), verbose: bool = False, jobs: int = 0) -> str
     return out
 
 
+def build_calib(out: str = CALIB_LIB) -> str:
+    """Compile and link the stream-read library (one translation unit)."""
+    cmd = [hipcc(), *COMPILE_FLAGS, f"-I{INCLUDE}", "-shared", "-o", out + ".tmp", CALIB_SRC]
+    rc, msgs = _run(cmd)
+    if rc != 0:
+        raise RuntimeError("hipcc failed:\n" + "\n".join(msgs))
+    os.replace(out + ".tmp", out)
+    return out
+
+
 if __name__ == "__main__":
     print(build(verbose="-v" in sys.argv))
+    print(build_calib())
