@@ -1,7 +1,7 @@
 """The bench's algorithmic bytes per call, pinned to the oracle's gather.
 
-bench.call_bytes and bench.step_bytes state what a call must move at the
-least (each prompt row once however many cells read it, each cell's own
+bench.call_bytes, bench.step_bytes and bench.forked_bytes state what a
+call must move at the least (each prompt row once however many cells read it, each cell's own
 generated rows, q, out and lse).  Here the same total is counted from the
 oracle's source map instead: the distinct (cache, prompt slot) pairs that
 any computed cell reads (ZERO slots read nothing), plus every computed
@@ -108,3 +108,41 @@ def test_step_bytes_match_the_oracle_source_map(wi):
         total += len(prompt_rows) * row
         got = bench.step_bytes(w, layer, steps.tolist(), w.cells)
         assert got == total, (w.name, layer, got, total)
+
+
+@pytest.mark.parametrize("wi", [1, 3, 4, 6])
+def test_forked_bytes_match_the_oracle_source_map(wi):
+    """A forked sweep computes the trunk and the cells that have diverged
+    (L < N and step >= W); below its onset W a diverged cell's generated
+    rows are the trunk's (nothing is spliced before W, so the cell is the
+    clean run there), so each (owner, row) pair is read once.  Dormant
+    cells read nothing and still receive out and lse."""
+    w = small_workloads()[wi].with_(cells=((4, 0), (0, 0), (1, 4), (2, 16), (3, 2), (0, 8)))
+    lw = workloads.cell_lw(w)
+    N, trunk = w.n_layers, 0
+    e = w.elem_bytes
+    row = 2 * w.n_kv_heads * w.head_dim * e
+    for layer in range(N):
+        A = arrays(w, layer)
+        for step in (0, 3, 4, 9, 16, w.n_steps - 1):
+            div = [c for c, (L, W) in enumerate(w.cells) if c == trunk or (L < N and step >= W)]
+            shape = oracle.shape_of(w)
+            _, _, src = oracle.gather(shape, layer, step, w.window(layer), lw, A["clean_k"], A["clean_v"],
+                                      A["donor_k"], A["donor_v"], A["gen_k"], A["gen_v"])
+            n_prompt = int(np.count_nonzero(src[0] != SRC_GEN))
+            jp0 = w.prompt_len - n_prompt
+            prompt_rows, gen_rows = set(), set()
+            for c in div:
+                n_gen = int(np.count_nonzero(src[c] == SRC_GEN))
+                for t in range(src.shape[1]):
+                    k = int(src[c, t])
+                    if k in (SRC_CLEAN, SRC_DONOR):
+                        prompt_rows.add((k, jp0 + t))
+                for r in range(step + 1 - n_gen, step + 1):
+                    owner = trunk if (c == trunk or r < w.cells[c][1]) else c
+                    gen_rows.add((owner, r))
+            want = (len(prompt_rows) + len(gen_rows)) * row
+            want += len(div) * w.n_q_heads * w.head_dim * e
+            want += w.n_cells * w.n_q_heads * (4 * w.head_dim + 4)
+            got = bench.forked_bytes(w, layer, step, list(w.cells), trunk)
+            assert got == want, (w.name, layer, step, got, want)
