@@ -455,6 +455,8 @@ def main():
     ap.add_argument("--no-e2e", action="store_true", help="skip the decode-loop measurement")
     ap.add_argument("--copy-calibration", type=int, default=0,
                     help="only run a plain device copy of this many MiB (counter calibration)")
+    ap.add_argument("--read-ceiling-only", action="store_true",
+                    help="only measure the stream-read ceiling and print it")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
@@ -483,6 +485,10 @@ def main():
             dst.copy_(src)
         torch.cuda.synchronize()
         print(json.dumps({"copy_calibration_bytes": n, "launches": 5}))
+        return
+
+    if args.read_ceiling_only:
+        print(json.dumps({"read_ceiling": read_ceiling(dev)}))
         return
 
     sp.load_library()
