@@ -39,8 +39,9 @@ Reported (one JSON line):
   read_ceiling  the rate of a plain stream read of a 4 GiB device buffer
               (libsplice_calib.so: contiguous parts per work group, 16-byte
               non-temporal loads; the best of three grid sizes, HIP events
-              over ten launches each), measured in the same process after
-              the timed region, and the sweep's GB/s as a share of it;
+              over ten launches each), measured in the same process before
+              anything else is allocated (the buffer stays allocated for the
+              run), and the sweep's GB/s as a share of it;
   decode_step  splice_decode_step passes (each cell at its own step, the
               current token's K/V appended, finished cells skipped) over two
               seeded step mixes -- 1/8 and 1/2 of the cells finished --
@@ -407,11 +408,14 @@ def sweep_summary(w, r, K: int):
 
 # ------------------------------------------------------------ read ceiling
 
-def read_ceiling(dev, gib: int = 4, reps: int = 10) -> dict:
+def read_ceiling(dev, gib: int = 4, reps: int = 10, keep: list = None) -> dict:
     """The rate of libsplice_calib.so's stream read over a `gib` GiB device
     buffer (16 times the last-level cache, so every launch reads from HBM):
     HIP events over `reps` launches after one untimed launch, for 1024, 2048
-    and 4096 work groups; the best of the three."""
+    and 4096 work groups; the best of the three.  Device memory handed out
+    again after a large free reads ~5% slower than a fresh allocation, so
+    the bench measures this first, on fresh memory, and keeps the buffer
+    (appended to `keep`) so that its own caches do not reuse that range."""
     import torch
 
     from paper_2605_30574_amd import calib
@@ -431,6 +435,8 @@ def read_ceiling(dev, gib: int = 4, reps: int = 10) -> dict:
         e1.record(stream)
         torch.cuda.synchronize()
         rates[blocks] = n * reps / (e0.elapsed_time(e1) / 1e3) / 1e9
+    if keep is not None:
+        keep.append(buf)
     del buf, sink
     torch.cuda.empty_cache()
     best = max(rates, key=rates.get)
@@ -492,6 +498,8 @@ def main():
         return
 
     sp.load_library()
+    held = []
+    ceiling = read_ceiling(dev, keep=held)
     w = workloads.get(args.config)
     N, S, C = w.n_layers, w.n_steps, w.n_cells
     K = args.steps if args.steps > 0 else S
@@ -712,9 +720,8 @@ def main():
     del sw, layers, qs, ws, out, lse, run
     torch.cuda.synchronize()
     torch.cuda.empty_cache()
-    ceiling = read_ceiling(dev)
-    log(f"stream-read ceiling: {ceiling['GB/s']} GB/s ({ceiling['blocks']} work groups); "
-        f"the sweep reaches {100 * gbs / ceiling['GB/s']:.1f}% of it")
+    log(f"stream-read ceiling (measured first, on fresh memory): {ceiling['GB/s']} GB/s "
+        f"({ceiling['blocks']} work groups); the sweep reaches {100 * gbs / ceiling['GB/s']:.1f}% of it")
     also = {}
     for name in [n for n in args.also.split(",") if n and n != w.name]:
         w2 = workloads.get(name)
